@@ -1,0 +1,159 @@
+/*
+ * prm.h -- C ABI of the Periodic Row-wise Muon (PRM) optimizer step for AMD
+ * MI355X (gfx950).  Library: libprm.so.
+ *
+ * The operation is Alg. 1 ("Periodic Row-wise Muon") of "Scaling Muon for
+ * Diffusion Transformers", applied to a fixed list of 2-D weight matrices on one
+ * GPU.  For every matrix W (m x n) with gradient G and momentum M, step t does
+ *
+ *   M <- beta*M + G                     (heavy-ball; optional dampening
+ *                                        M <- beta*M + (1-beta)*G)
+ *   U  = M, or G + beta*M with Nesterov
+ *   rho_t = 1[t mod K = 0]              (Sec. 3.3, eq. periodic-direction)
+ *   U~ = U if m <= n else U^T           (orientation, Sec. 3.1; r = min, c = max)
+ *   D~ = NS5(U~)                 if rho_t   (eq. app-ns-recurrence, five iterations of
+ *                                            G = XX^T, B = bG + cG^2, X <- aX + BX on
+ *                                            X0 = U~/(||U~||_F + eps_ns))
+ *      = gamma * RowNorm_eps(U~) otherwise  (eq. rownorm: row / max(||row||_2, eps))
+ *   D  = s(W) * O^{-1}(D~)
+ *   W <- (1 - eta*lambda)*W - eta*D     (eq. periodic-direction; Alg. 1)
+ *
+ * Numerics: momentum, RowNorm and the parameter write are fp32; NS5 runs as
+ * bf16-input / fp32-accumulate matrix products (MFMA) with the Gram matrix
+ * carried as a bf16 hi + lo pair; W is rounded to its storage type (RNE).
+ *
+ * Memory: every matrix buffer is a DEVICE pointer to a contiguous row-major
+ * m x n array owned by the caller.  W and M are updated in place, G is only
+ * read.  Buffers of different matrices, and W / G / M of one matrix, must not
+ * overlap.  Pointer arrays (the `const*` arguments) are HOST arrays read
+ * during the call only.  The library owns its workspace (allocated by
+ * prm_init, freed by prm_destroy) and never frees caller memory.
+ *
+ * Streams: prm_step and prm_step_debug only enqueue work on the stream given
+ * to prm_init (a hipStream_t; NULL = the default stream) and never wait for
+ * the GPU, except that a call whose pointer arrays differ from the previous
+ * call's waits for that previous call's small pointer-table upload to finish.
+ *
+ * Errors: every entry point returns PRM_OK (0) or a negative PRM_E* code and
+ * stores a message readable with prm_last_error() (per thread).  Arguments are
+ * validated before anything is enqueued, so a failed call has no effect on
+ * the caller's buffers.  A context is not thread-safe; separate contexts are.
+ */
+#ifndef PRM_H
+#define PRM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PRM_OK 0
+#define PRM_EINVAL (-1)  /* bad argument: K < 1, beta outside [0,1), shape < 1, NULL, t < 0, ... */
+#define PRM_EDTYPE (-2)  /* unsupported storage type */
+#define PRM_EALIGN (-3)  /* a device pointer is not 16-byte aligned */
+#define PRM_ENOMEM (-4)  /* workspace does not fit the budget or the device */
+#define PRM_EHIP   (-5)  /* a HIP runtime call failed; the message carries its error string */
+
+typedef enum prm_dtype { PRM_F32 = 0, PRM_BF16 = 1 } prm_dtype;
+
+/* Shape scale s(W) of eq. (periodic-direction); the paper names it a
+ * "shape-dependent update scale" without a formula. */
+typedef enum prm_scale_mode {
+  PRM_SCALE_ONE = 0,          /* s = 1 */
+  PRM_SCALE_SQRT_ASPECT = 1,  /* s = sqrt(max(1, m/n)) (default) */
+  PRM_SCALE_RMS_0P2 = 2       /* s = 0.2 * sqrt(max(m, n)) */
+} prm_scale_mode;
+
+typedef struct prm_config {
+  int32_t K;             /* refresh period, >= 1 (Sec. 3.3) */
+  float beta;            /* momentum, in [0, 1) */
+  float lr;              /* eta used when prm_step gets lr < 0; >= 0 */
+  float wd;              /* decoupled weight decay lambda, >= 0 */
+  float gamma;           /* RowNorm multiplier (> 0); scales only the RowNorm branch */
+  float eps_rownorm;     /* RowNorm clamp, > 0 (applied after the square root) */
+  float eps_ns;          /* NS input normalization X0 = U/(||U||_F + eps_ns), >= 0 */
+  float ns_a, ns_b, ns_c;/* quintic coefficients (3.4445, -4.7750, 2.0315) */
+  int32_t nesterov;      /* 0: U = M;  1: U = G + beta*M (after the momentum update) */
+  int32_t ema_dampening; /* 0: M = beta*M + G;  1: M = beta*M + (1-beta)*G */
+  int32_t scale_mode;    /* prm_scale_mode */
+  int32_t param_dtype;   /* prm_dtype of W (momentum is always fp32) */
+  int32_t grad_dtype;    /* prm_dtype of G */
+  int32_t never_refresh; /* ablation: RowNorm on every step (K ignored) */
+  int32_t gamma_on_refresh; /* ablation: gamma also scales the NS5 direction */
+  int32_t reserved;
+  uint64_t workspace_budget_bytes; /* NS5 workspace cap; 0 = automatic */
+} prm_config;
+
+typedef struct prm_ctx prm_ctx; /* opaque */
+
+/* Fill *cfg with the paper's defaults: K = 3, beta = 0.95, lr = 5e-3,
+ * wd = 0.01, gamma = 0.15 (optimizer hyperparameter table), eps_rownorm = 1e-8,
+ * eps_ns = 1e-7, (a,b,c) = (3.4445, -4.7750, 2.0315), heavy-ball momentum,
+ * s = sqrt(max(1, m/n)), bf16 W and G. */
+void prm_config_default(prm_config* cfg);
+
+/* Create a context for n_mats matrices of shapes rows[i] x cols[i] (host
+ * arrays, each >= 1; n_mats >= 0).  Validates cfg, groups the matrices by
+ * oriented NS5 shape, plans and allocates the device workspace (hipMalloc on
+ * the current device) and records `hip_stream` for later calls.
+ * On success *out owns the workspace until prm_destroy. */
+int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* cols,
+             const prm_config* cfg, void* hip_stream);
+
+/* One optimizer step t (0-based, >= 0) over every matrix, enqueued on the
+ * context's stream.  params[i]: W (param_dtype), grads[i]: G (grad_dtype),
+ * momentum[i]: M (fp32); all device pointers, 16-byte aligned.  lr < 0 uses
+ * cfg->lr.  *did_refresh (nullable) receives rho_t, computed on the host. */
+int prm_step(prm_ctx* ctx, void* const* params, const void* const* grads,
+             float* const* momentum, int64_t step, float lr, int32_t* did_refresh);
+
+/* prm_step that also writes D = s(W) * O^{-1}(D~) (fp32, m x n, row-major,
+ * device) for every matrix into direction_out[i].  Parity checking only. */
+int prm_step_debug(prm_ctx* ctx, void* const* params, const void* const* grads,
+                   float* const* momentum, int64_t step, float lr, int32_t* did_refresh,
+                   float* const* direction_out);
+
+/* rho_t = 1[t mod K = 0] (Sec. 3.3): 1 or 0, or PRM_EINVAL for K < 1 or t < 0.
+ * Pure host function. */
+int prm_is_refresh(int64_t step, int32_t K);
+
+/* Device bytes prm_init would allocate for these shapes and cfg (pure host
+ * planning, no device call). */
+int prm_workspace_bytes(int32_t n_mats, const int64_t* rows, const int64_t* cols,
+                        const prm_config* cfg, uint64_t* out_bytes);
+
+/* Per-kernel-class timing on the context's stream, for measurement.
+ * prm_profile_enable(ctx, 1) makes later steps record a HIP event pair around
+ * every kernel launch (on the same stream); prm_profile_read synchronizes the
+ * stream and fills out[0 .. min(n, PRM_NUM_KERNEL_CLASSES)) with, per kernel
+ * class, the launch count, total GPU milliseconds, and the algorithmic bytes
+ * and FLOPs of those launches, then clears the counters.  Classes, in order:
+ * rw_wide, rw_generic, rw_tall_stats, rw_tall_finalize, rw_tall_apply,
+ * ns_prologue, ns_alpha, ns_gram, ns_poly, ns_apply.  Algorithmic bytes count
+ * each element of G, M and W once per read or write the method needs (the
+ * tall-matrix re-read of M is not counted); algorithmic FLOPs are the paper's
+ * 2r^2c (Gram), 2r^3 (square) and 2r^2c (apply) per matrix and iteration. */
+#define PRM_NUM_KERNEL_CLASSES 10
+typedef struct prm_kernel_stats {
+  char name[32];
+  int64_t launches;
+  double total_ms;
+  double alg_bytes;
+  double alg_flops;
+} prm_kernel_stats;
+int prm_profile_enable(prm_ctx* ctx, int32_t enable);
+int prm_profile_read(prm_ctx* ctx, prm_kernel_stats* out, int32_t n);
+
+/* Free the workspace (after synchronizing the context's stream) and the
+ * context.  NULL is a no-op. */
+int prm_destroy(prm_ctx* ctx);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* prm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PRM_H */

@@ -1,0 +1,711 @@
+// C ABI and host dispatcher of libprm (declared in include/prm.h).
+//
+// prm_init plans once: orientation and shape scale per matrix, the row-wise
+// launch classes (row length -> threads per row and chunks per thread), the
+// tall-matrix work lists, and the NS5 chunks (matrices grouped by oriented
+// shape, packed into a bounded workspace) with their tile work lists.
+// prm_step then only enqueues kernels on the context's stream: the refresh
+// indicator rho_t = 1[t mod K = 0] (Sec. 3.3, Alg. 1) is decided on the host.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/prm.h"
+#include "prm_internal.h"
+
+using namespace prm;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                    \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail(PRM_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));              \
+  } while (0)
+
+constexpr uint64_t kAutoBudget = 32ull << 30;  // NS5 chunk workspace cap when unset
+constexpr int64_t kMaxDim = 1ll << 24;
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+
+enum KClass {
+  K_RW_WIDE = 0, K_RW_GENERIC, K_RW_TALL_STATS, K_RW_TALL_FIN, K_RW_TALL_APPLY,
+  K_NS_PROLOGUE, K_NS_ALPHA, K_NS_GRAM, K_NS_POLY, K_NS_APPLY, K_NCLASS
+};
+static_assert(K_NCLASS == PRM_NUM_KERNEL_CLASSES, "kernel class table");
+const char* kClassName[K_NCLASS] = {"rw_wide", "rw_generic", "rw_tall_stats",
+                                    "rw_tall_finalize", "rw_tall_apply", "ns_prologue",
+                                    "ns_alpha", "ns_gram", "ns_poly", "ns_apply"};
+
+struct WideClass {
+  int tpr, nch;
+  std::vector<int32_t> mats, starts;
+  int32_t nblocks = 0;
+  size_t off_mats = 0, off_starts = 0;
+  double elems = 0;
+};
+
+struct Chunk {
+  std::vector<int32_t> mats;
+  std::vector<Item> prologue, gram, poly, apply;
+  size_t off_mats = 0, off_prologue = 0, off_gram = 0, off_poly = 0, off_apply = 0;
+  double elems = 0, flops_gram = 0, flops_poly = 0, flops_apply = 0;
+};
+
+struct Plan {
+  int32_t n = 0;
+  std::vector<int64_t> m, nn, rp, cp;
+  std::vector<int32_t> tall;
+  std::vector<float> s;
+  std::vector<uint64_t> ws_off;     // offset of the matrix's NS region inside the chunk area
+  std::vector<uint64_t> small_off;  // partial sums + alpha
+  std::vector<uint64_t> tall_off;   // colpart + colinv
+  std::vector<int32_t> nrb;
+  uint64_t chunk_bytes = 0, small_bytes = 0, tall_bytes = 0, total_bytes = 0;
+  std::vector<WideClass> wide;
+  WideClass generic;
+  std::vector<Item> tall_items4, tall_items1, fin_items;
+  size_t off_tall4 = 0, off_tall1 = 0, off_fin = 0;
+  double tall_elems4 = 0, tall_elems1 = 0;
+  std::vector<Chunk> chunks;
+  std::vector<int32_t> ints;   // all int32 lists, uploaded once
+  std::vector<Item> items;     // all item lists, uploaded once
+};
+
+int validate_cfg(const prm_config* c) {
+  if (!c) return fail(PRM_EINVAL, "cfg is NULL");
+  if (c->K < 1) return fail(PRM_EINVAL, "K must be >= 1 (got %d)", c->K);
+  if (!(c->beta >= 0.f && c->beta < 1.f)) return fail(PRM_EINVAL, "beta must be in [0,1)");
+  if (!(c->lr >= 0.f) || !std::isfinite(c->lr)) return fail(PRM_EINVAL, "lr must be finite and >= 0");
+  if (!(c->wd >= 0.f) || !std::isfinite(c->wd)) return fail(PRM_EINVAL, "wd must be finite and >= 0");
+  if (!(c->gamma > 0.f) || !std::isfinite(c->gamma)) return fail(PRM_EINVAL, "gamma must be > 0");
+  if (!(c->eps_rownorm > 0.f)) return fail(PRM_EINVAL, "eps_rownorm must be > 0");
+  if (!(c->eps_ns >= 0.f)) return fail(PRM_EINVAL, "eps_ns must be >= 0");
+  if (!std::isfinite(c->ns_a) || !std::isfinite(c->ns_b) || !std::isfinite(c->ns_c))
+    return fail(PRM_EINVAL, "NS coefficients must be finite");
+  if (c->nesterov != 0 && c->nesterov != 1) return fail(PRM_EINVAL, "nesterov must be 0 or 1");
+  if (c->ema_dampening != 0 && c->ema_dampening != 1) return fail(PRM_EINVAL, "ema_dampening must be 0 or 1");
+  if (c->never_refresh != 0 && c->never_refresh != 1) return fail(PRM_EINVAL, "never_refresh must be 0 or 1");
+  if (c->gamma_on_refresh != 0 && c->gamma_on_refresh != 1) return fail(PRM_EINVAL, "gamma_on_refresh must be 0 or 1");
+  if (c->scale_mode < 0 || c->scale_mode > 2) return fail(PRM_EINVAL, "unknown scale_mode %d", c->scale_mode);
+  if (c->param_dtype != PRM_F32 && c->param_dtype != PRM_BF16) return fail(PRM_EDTYPE, "unsupported param_dtype %d", c->param_dtype);
+  if (c->grad_dtype != PRM_F32 && c->grad_dtype != PRM_BF16) return fail(PRM_EDTYPE, "unsupported grad_dtype %d", c->grad_dtype);
+  return PRM_OK;
+}
+
+float shape_scale(int64_t m, int64_t n, int mode) {
+  switch (mode) {
+    case PRM_SCALE_ONE: return 1.0f;
+    case PRM_SCALE_RMS_0P2: return (float)(0.2 * std::sqrt((double)std::max(m, n)));
+    default: return (float)std::sqrt(std::max(1.0, (double)m / (double)n));
+  }
+}
+
+// NS5 workspace of one matrix: X, XT and the next iterate in both layouts
+// (bf16), off-diagonal A and B (bf16), diagonals of A and B (fp32).
+uint64_t ns_matrix_bytes(int64_t rp, int64_t cp) {
+  const uint64_t xs = align256((uint64_t)rp * cp * 2), gs = align256((uint64_t)rp * rp * 2),
+                 vs = align256((uint64_t)rp * 4);
+  return 4 * xs + 2 * gs + 2 * vs;
+}
+
+// Row-wise launch class of a wide row of length n (0 tpr = generic path).
+void wide_class(int64_t n, int& tpr, int& nch) {
+  tpr = 0;
+  nch = 0;
+  if (n % 8 != 0) return;
+  const int64_t chunks = n / 8;
+  if (chunks <= 64 * 8) { tpr = 64; nch = (int)((chunks + 63) / 64); }
+  else if (chunks <= 256 * 8) { tpr = 256; nch = (int)((chunks + 255) / 256); }
+  else if (chunks <= 512 * 8) { tpr = 512; nch = (int)((chunks + 511) / 512); }
+}
+
+int make_plan(int32_t n_mats, const int64_t* rows, const int64_t* cols, const prm_config* cfg,
+              Plan& P) {
+  int rc = validate_cfg(cfg);
+  if (rc) return rc;
+  if (n_mats < 0) return fail(PRM_EINVAL, "n_mats must be >= 0");
+  if (n_mats > 0 && (!rows || !cols)) return fail(PRM_EINVAL, "rows/cols is NULL");
+  P = Plan();
+  P.n = n_mats;
+  const int wb = cfg->param_dtype == PRM_BF16 ? 2 : 4;
+  (void)wb;
+  for (int i = 0; i < n_mats; ++i) {
+    const int64_t m = rows[i], n = cols[i];
+    if (m < 1 || n < 1 || m > kMaxDim || n > kMaxDim)
+      return fail(PRM_EINVAL, "matrix %d has invalid shape %lld x %lld", i, (long long)m, (long long)n);
+    const int64_t r = std::min(m, n), c = std::max(m, n);
+    P.m.push_back(m);
+    P.nn.push_back(n);
+    P.tall.push_back(m > n ? 1 : 0);
+    P.rp.push_back(round_up(r, kNsTile));
+    P.cp.push_back(round_up(c, kNsTile));
+    P.s.push_back(shape_scale(m, n, cfg->scale_mode));
+  }
+  // ---- small persistent buffers: prologue partial sums + alpha per matrix ----
+  uint64_t off = 0;
+  P.small_off.resize(n_mats);
+  for (int i = 0; i < n_mats; ++i) {
+    const int64_t pt = (P.rp[i] / kPrologueTile) * (P.cp[i] / kPrologueTile);
+    P.small_off[i] = off;
+    off = align256(off + (uint64_t)(pt + 1) * 4);
+  }
+  P.small_bytes = off;
+  // ---- tall buffers ----
+  off = 0;
+  P.tall_off.assign(n_mats, 0);
+  P.nrb.assign(n_mats, 0);
+  for (int i = 0; i < n_mats; ++i) {
+    if (!P.tall[i]) continue;
+    const int64_t nrb = (P.m[i] + kTallRows - 1) / kTallRows;
+    P.nrb[i] = (int32_t)nrb;
+    P.tall_off[i] = off;
+    off = align256(off + (uint64_t)(nrb + 1) * P.nn[i] * 4);
+  }
+  P.tall_bytes = off;
+  // ---- NS5 chunks: group by oriented padded shape, largest first ----
+  const uint64_t budget = cfg->workspace_budget_bytes ? cfg->workspace_budget_bytes : kAutoBudget;
+  std::vector<int32_t> order(n_mats);
+  for (int i = 0; i < n_mats; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+    if (P.rp[a] != P.rp[b]) return P.rp[a] > P.rp[b];
+    return P.cp[a] > P.cp[b];
+  });
+  P.ws_off.assign(n_mats, 0);
+  uint64_t cur = 0;
+  for (int idx : order) {
+    const uint64_t need = ns_matrix_bytes(P.rp[idx], P.cp[idx]);
+    if (need > budget)
+      return fail(PRM_ENOMEM, "matrix %d needs %llu workspace bytes, budget is %llu", idx,
+                  (unsigned long long)need, (unsigned long long)budget);
+    if (P.chunks.empty() || cur + need > budget) {
+      P.chunks.emplace_back();
+      cur = 0;
+    }
+    P.chunks.back().mats.push_back(idx);
+    P.ws_off[idx] = cur;
+    cur += need;
+    P.chunk_bytes = std::max(P.chunk_bytes, cur);
+  }
+  P.total_bytes = align256(P.chunk_bytes) + P.small_bytes + P.tall_bytes;
+  return PRM_OK;
+}
+
+// Work lists (host side); built only by prm_init.
+void build_lists(Plan& P, const prm_config* cfg) {
+  // row-wise wide classes
+  for (int i = 0; i < P.n; ++i) {
+    if (P.tall[i]) continue;
+    int tpr, nch;
+    wide_class(P.nn[i], tpr, nch);
+    WideClass* wc = nullptr;
+    if (tpr == 0) {
+      wc = &P.generic;
+    } else {
+      for (auto& w : P.wide)
+        if (w.tpr == tpr && w.nch == nch) wc = &w;
+      if (!wc) {
+        P.wide.emplace_back();
+        wc = &P.wide.back();
+        wc->tpr = tpr;
+        wc->nch = nch;
+      }
+    }
+    const int rpb = (tpr == 64) ? 4 : 1;
+    wc->mats.push_back(i);
+    wc->starts.push_back(wc->nblocks);
+    wc->nblocks += (int32_t)((P.m[i] + rpb - 1) / rpb);
+    wc->elems += (double)P.m[i] * P.nn[i];
+  }
+  // tall lists
+  for (int i = 0; i < P.n; ++i) {
+    if (!P.tall[i]) continue;
+    const int vec = (P.nn[i] % 4 == 0) ? 4 : 1;
+    const int64_t slabs = (P.nn[i] + 256 * vec - 1) / (256 * vec);
+    auto& L = vec == 4 ? P.tall_items4 : P.tall_items1;
+    for (int32_t rb = 0; rb < P.nrb[i]; ++rb)
+      for (int32_t sb = 0; sb < slabs; ++sb) L.push_back(Item{i, rb, sb, 0});
+    (vec == 4 ? P.tall_elems4 : P.tall_elems1) += (double)P.m[i] * P.nn[i];
+    for (int32_t cb = 0; cb < (P.nn[i] + 255) / 256; ++cb) P.fin_items.push_back(Item{i, 0, cb, 0});
+  }
+  // NS5 lists per chunk
+  for (auto& ch : P.chunks) {
+    for (int i : ch.mats) {
+      const int64_t pm = (P.tall[i] ? P.cp[i] : P.rp[i]) / kPrologueTile;
+      const int64_t pn = (P.tall[i] ? P.rp[i] : P.cp[i]) / kPrologueTile;
+      for (int32_t a = 0; a < pm; ++a)
+        for (int32_t b = 0; b < pn; ++b) ch.prologue.push_back(Item{i, a, b, 0});
+      const int32_t tr = (int32_t)(P.rp[i] / kNsTile), tc = (int32_t)(P.cp[i] / kNsTile);
+      for (int32_t a = 0; a < tr; ++a)
+        for (int32_t b = a; b < tr; ++b) {
+          ch.gram.push_back(Item{i, a, b, 0});
+          ch.poly.push_back(Item{i, a, b, 0});
+        }
+      for (int32_t a = 0; a < tr; ++a)
+        for (int32_t b = 0; b < tc; ++b) ch.apply.push_back(Item{i, a, b, 0});
+      const double r = (double)std::min(P.m[i], P.nn[i]), c = (double)std::max(P.m[i], P.nn[i]);
+      ch.elems += r * c;
+      ch.flops_gram += 2 * r * r * c;
+      ch.flops_poly += 2 * r * r * r;
+      ch.flops_apply += 2 * r * r * c;
+    }
+  }
+  (void)cfg;
+  // flatten
+  auto put_ints = [&](const std::vector<int32_t>& v) {
+    size_t o = P.ints.size();
+    P.ints.insert(P.ints.end(), v.begin(), v.end());
+    return o;
+  };
+  auto put_items = [&](const std::vector<Item>& v) {
+    size_t o = P.items.size();
+    P.items.insert(P.items.end(), v.begin(), v.end());
+    return o;
+  };
+  for (auto& w : P.wide) {
+    w.off_mats = put_ints(w.mats);
+    w.off_starts = put_ints(w.starts);
+  }
+  P.generic.off_mats = put_ints(P.generic.mats);
+  P.generic.off_starts = put_ints(P.generic.starts);
+  P.off_tall4 = put_items(P.tall_items4);
+  P.off_tall1 = put_items(P.tall_items1);
+  P.off_fin = put_items(P.fin_items);
+  for (auto& ch : P.chunks) {
+    ch.off_mats = put_ints(ch.mats);
+    ch.off_prologue = put_items(ch.prologue);
+    ch.off_gram = put_items(ch.gram);
+    ch.off_poly = put_items(ch.poly);
+    ch.off_apply = put_items(ch.apply);
+  }
+  if (P.ints.empty()) P.ints.push_back(0);
+  if (P.items.empty()) P.items.push_back(Item{0, 0, 0, 0});
+}
+
+struct ProfRec {
+  int cls;
+  hipEvent_t e0, e1;
+  double bytes, flops;
+};
+
+}  // namespace
+
+struct prm_ctx {
+  prm_config cfg;
+  Plan plan;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  char* d_ws = nullptr;
+  MatDesc* d_desc = nullptr;
+  MatDesc* h_desc = nullptr;  // pinned staging of the descriptor table
+  int32_t* d_ints = nullptr;
+  Item* d_items = nullptr;
+  hipEvent_t upload_done = nullptr;
+  bool uploaded = false;
+  bool debug_last = false;
+  std::vector<const void*> last_ptrs;
+  std::vector<MatDesc> desc;  // host copy (workspace fields filled at init)
+  // profiling
+  bool prof = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+  size_t pool_used = 0;
+};
+
+namespace {
+
+hipEvent_t take_event(prm_ctx* c) {
+  if (c->pool_used == c->pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->pool.push_back(e);
+  }
+  return c->pool[c->pool_used++];
+}
+
+// Run `launch` on the context stream, bracketed by events when profiling.
+template <typename F>
+int timed(prm_ctx* c, int cls, double bytes, double flops, F&& launch) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (c->prof) {
+    e0 = take_event(c);
+    e1 = take_event(c);
+    if (!e0 || !e1) return fail(PRM_EHIP, "hipEventCreate failed");
+    HIP_TRY(hipEventRecord(e0, c->stream));
+  }
+  hipError_t e = launch();
+  if (e != hipSuccess) return fail(PRM_EHIP, "%s launch failed: %s", kClassName[cls], hipGetErrorString(e));
+  if (c->prof) {
+    HIP_TRY(hipEventRecord(e1, c->stream));
+    c->recs.push_back(ProfRec{cls, e0, e1, bytes, flops});
+  }
+  return PRM_OK;
+}
+
+int upload_desc(prm_ctx* c, void* const* params, const void* const* grads,
+                float* const* momentum, float* const* dirs) {
+  const int n = c->plan.n;
+  bool same = c->uploaded && c->debug_last == (dirs != nullptr);
+  if (same) {
+    for (int i = 0; i < n && same; ++i)
+      same = c->last_ptrs[4 * i] == params[i] && c->last_ptrs[4 * i + 1] == grads[i] &&
+             c->last_ptrs[4 * i + 2] == momentum[i] &&
+             c->last_ptrs[4 * i + 3] == (dirs ? (const void*)dirs[i] : nullptr);
+  }
+  if (same) return PRM_OK;
+  if (c->uploaded) HIP_TRY(hipEventSynchronize(c->upload_done));
+  for (int i = 0; i < n; ++i) {
+    MatDesc& d = c->desc[i];
+    d.W = params[i];
+    d.G = grads[i];
+    d.M = momentum[i];
+    d.D = dirs ? dirs[i] : nullptr;
+    c->last_ptrs[4 * i] = params[i];
+    c->last_ptrs[4 * i + 1] = grads[i];
+    c->last_ptrs[4 * i + 2] = momentum[i];
+    c->last_ptrs[4 * i + 3] = dirs ? (const void*)dirs[i] : nullptr;
+  }
+  std::memcpy(c->h_desc, c->desc.data(), sizeof(MatDesc) * n);
+  HIP_TRY(hipMemcpyAsync(c->d_desc, c->h_desc, sizeof(MatDesc) * n, hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(hipEventRecord(c->upload_done, c->stream));
+  c->uploaded = true;
+  c->debug_last = dirs != nullptr;
+  return PRM_OK;
+}
+
+int rowwise_step(prm_ctx* c, float lr, bool debug) {
+  const Plan& P = c->plan;
+  const prm_config& cf = c->cfg;
+  RwParams p;
+  p.beta = cf.beta;
+  p.gcoef = cf.ema_dampening ? 1.0f - cf.beta : 1.0f;
+  p.lr = lr;
+  p.decay = 1.0f - lr * cf.wd;
+  p.gamma = cf.gamma;
+  p.eps = cf.eps_rownorm;
+  p.nesterov = cf.nesterov;
+  p.write_d = debug ? 1 : 0;
+  const DType wt = (DType)cf.param_dtype, gt = (DType)cf.grad_dtype;
+  const double gb = gt == BF16 ? 2 : 4, wb = wt == BF16 ? 2 : 4, db = debug ? 4 : 0;
+  const MatDesc* md = c->d_desc;
+  int rc;
+  // tall matrices first (column statistics, then their parameter write)
+  for (int v : {4, 1}) {
+    const auto& L = v == 4 ? P.tall_items4 : P.tall_items1;
+    if (L.empty()) continue;
+    const Item* items = c->d_items + (v == 4 ? P.off_tall4 : P.off_tall1);
+    const double el = v == 4 ? P.tall_elems4 : P.tall_elems1;
+    rc = timed(c, K_RW_TALL_STATS, el * (gb + 8), 0, [&] {
+      return launch_rw_tall_stats(v, gt, md, items, (int32_t)L.size(), p, c->stream);
+    });
+    if (rc) return rc;
+  }
+  if (!P.fin_items.empty()) {
+    rc = timed(c, K_RW_TALL_FIN, 0, 0, [&] {
+      return launch_rw_tall_finalize(md, c->d_items + P.off_fin, (int32_t)P.fin_items.size(), p, c->stream);
+    });
+    if (rc) return rc;
+  }
+  for (int v : {4, 1}) {
+    const auto& L = v == 4 ? P.tall_items4 : P.tall_items1;
+    if (L.empty()) continue;
+    const Item* items = c->d_items + (v == 4 ? P.off_tall4 : P.off_tall1);
+    const double el = v == 4 ? P.tall_elems4 : P.tall_elems1;
+    rc = timed(c, K_RW_TALL_APPLY, el * (2 * wb + db), 0, [&] {
+      return launch_rw_tall_apply(v, wt, gt, md, items, (int32_t)L.size(), p, c->stream);
+    });
+    if (rc) return rc;
+  }
+  for (const auto& w : P.wide) {
+    rc = timed(c, K_RW_WIDE, w.elems * (gb + 8 + 2 * wb + db), 0, [&] {
+      return launch_rw_wide(w.tpr, w.nch, wt, gt, md, c->d_ints + w.off_mats,
+                            c->d_ints + w.off_starts, (int32_t)w.mats.size(), w.nblocks, p,
+                            c->stream);
+    });
+    if (rc) return rc;
+  }
+  if (!P.generic.mats.empty()) {
+    const auto& w = P.generic;
+    rc = timed(c, K_RW_GENERIC, w.elems * (gb + 8 + 2 * wb + db), 0, [&] {
+      return launch_rw_generic(wt, gt, md, c->d_ints + w.off_mats, c->d_ints + w.off_starts,
+                               (int32_t)w.mats.size(), w.nblocks, p, c->stream);
+    });
+    if (rc) return rc;
+  }
+  return PRM_OK;
+}
+
+int refresh_step(prm_ctx* c, float lr, bool debug) {
+  const Plan& P = c->plan;
+  const prm_config& cf = c->cfg;
+  NsParams p;
+  p.beta = cf.beta;
+  p.gcoef = cf.ema_dampening ? 1.0f - cf.beta : 1.0f;
+  p.nesterov = cf.nesterov;
+  p.eps_ns = cf.eps_ns;
+  p.a = cf.ns_a;
+  p.b = cf.ns_b;
+  p.c = cf.ns_c;
+  p.lr = lr;
+  p.decay = 1.0f - lr * cf.wd;
+  p.dscale = cf.gamma_on_refresh ? cf.gamma : 1.0f;
+  p.write_d = debug ? 1 : 0;
+  const DType wt = (DType)cf.param_dtype, gt = (DType)cf.grad_dtype;
+  const double gb = gt == BF16 ? 2 : 4, wb = wt == BF16 ? 2 : 4, db = debug ? 4 : 0;
+  const MatDesc* md = c->d_desc;
+  constexpr int kIters = 5;
+  int rc;
+  for (const auto& ch : P.chunks) {
+    p.iter = 0;
+    p.last = 0;
+    rc = timed(c, K_NS_PROLOGUE, ch.elems * (gb + 8 + 4), 0, [&] {
+      return launch_ns_prologue(gt, md, c->d_items + ch.off_prologue, (int32_t)ch.prologue.size(), p, c->stream);
+    });
+    if (rc) return rc;
+    rc = timed(c, K_NS_ALPHA, 0, 0, [&] {
+      return launch_ns_alpha(md, c->d_ints + ch.off_mats, (int32_t)ch.mats.size(), p, c->stream);
+    });
+    if (rc) return rc;
+    for (int j = 0; j < kIters; ++j) {
+      p.iter = j;
+      p.last = (j == kIters - 1) ? 1 : 0;
+      rc = timed(c, K_NS_GRAM, 0, ch.flops_gram, [&] {
+        return launch_ns_gemm(GEMM_GRAM, wt, md, c->d_items + ch.off_gram, (int32_t)ch.gram.size(), p, c->stream);
+      });
+      if (rc) return rc;
+      rc = timed(c, K_NS_POLY, 0, ch.flops_poly, [&] {
+        return launch_ns_gemm(GEMM_POLY, wt, md, c->d_items + ch.off_poly, (int32_t)ch.poly.size(), p, c->stream);
+      });
+      if (rc) return rc;
+      rc = timed(c, K_NS_APPLY, p.last ? ch.elems * (2 * wb + db) : 0, ch.flops_apply, [&] {
+        return launch_ns_gemm(GEMM_APPLY, wt, md, c->d_items + ch.off_apply, (int32_t)ch.apply.size(), p, c->stream);
+      });
+      if (rc) return rc;
+    }
+  }
+  return PRM_OK;
+}
+
+int do_step(prm_ctx* c, void* const* params, const void* const* grads, float* const* momentum,
+            int64_t t, float lr, int32_t* did_refresh, float* const* dirs, bool debug) {
+  if (!c) return fail(PRM_EINVAL, "ctx is NULL");
+  if (t < 0) return fail(PRM_EINVAL, "step must be >= 0 (got %lld)", (long long)t);
+  const float eta = lr < 0.f ? c->cfg.lr : lr;
+  if (!std::isfinite(eta)) return fail(PRM_EINVAL, "lr must be finite");
+  const int n = c->plan.n;
+  if (n > 0 && (!params || !grads || !momentum))
+    return fail(PRM_EINVAL, "params/grads/momentum array is NULL");
+  if (debug && n > 0 && !dirs) return fail(PRM_EINVAL, "direction_out array is NULL");
+  for (int i = 0; i < n; ++i) {
+    const void* ps[4] = {params[i], grads[i], momentum[i], debug ? (const void*)dirs[i] : nullptr};
+    for (int k = 0; k < (debug ? 4 : 3); ++k) {
+      if (!ps[k]) return fail(PRM_EINVAL, "matrix %d: NULL device pointer (argument %d)", i, k);
+      if ((uintptr_t)ps[k] % 16) return fail(PRM_EALIGN, "matrix %d: pointer %d is not 16-byte aligned", i, k);
+    }
+  }
+  const int rho = c->cfg.never_refresh ? 0 : (t % c->cfg.K == 0 ? 1 : 0);
+  if (did_refresh) *did_refresh = rho;
+  if (n == 0) return PRM_OK;
+  HIP_TRY(hipSetDevice(c->device));
+  int rc = upload_desc(c, params, grads, momentum, debug ? dirs : nullptr);
+  if (rc) return rc;
+  return rho ? refresh_step(c, eta, debug) : rowwise_step(c, eta, debug);
+}
+
+}  // namespace
+
+extern "C" {
+
+void prm_config_default(prm_config* cfg) {
+  if (!cfg) return;
+  std::memset(cfg, 0, sizeof(*cfg));
+  cfg->K = 3;
+  cfg->beta = 0.95f;
+  cfg->lr = 5e-3f;
+  cfg->wd = 0.01f;
+  cfg->gamma = 0.15f;
+  cfg->eps_rownorm = 1e-8f;
+  cfg->eps_ns = 1e-7f;
+  cfg->ns_a = 3.4445f;
+  cfg->ns_b = -4.7750f;
+  cfg->ns_c = 2.0315f;
+  cfg->scale_mode = PRM_SCALE_SQRT_ASPECT;
+  cfg->param_dtype = PRM_BF16;
+  cfg->grad_dtype = PRM_BF16;
+}
+
+int prm_is_refresh(int64_t step, int32_t K) {
+  if (K < 1) return fail(PRM_EINVAL, "K must be >= 1 (got %d)", K);
+  if (step < 0) return fail(PRM_EINVAL, "step must be >= 0 (got %lld)", (long long)step);
+  return step % K == 0 ? 1 : 0;
+}
+
+int prm_workspace_bytes(int32_t n_mats, const int64_t* rows, const int64_t* cols,
+                        const prm_config* cfg, uint64_t* out_bytes) {
+  if (!out_bytes) return fail(PRM_EINVAL, "out_bytes is NULL");
+  Plan P;
+  int rc = make_plan(n_mats, rows, cols, cfg, P);
+  if (rc) return rc;
+  *out_bytes = P.total_bytes;
+  return PRM_OK;
+}
+
+int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* cols,
+             const prm_config* cfg, void* hip_stream) {
+  if (!out) return fail(PRM_EINVAL, "out is NULL");
+  *out = nullptr;
+  prm_ctx* c = new prm_ctx();
+  int rc = make_plan(n_mats, rows, cols, cfg, c->plan);
+  if (rc) {
+    delete c;
+    return rc;
+  }
+  c->cfg = *cfg;
+  c->stream = (hipStream_t)hip_stream;
+  build_lists(c->plan, cfg);
+  Plan& P = c->plan;
+  auto cleanup = [&](int code) {
+    prm_destroy(c);
+    return code;
+  };
+  hipError_t e = hipGetDevice(&c->device);
+  if (e != hipSuccess) return cleanup(fail(PRM_EHIP, "hipGetDevice failed: %s", hipGetErrorString(e)));
+  if (P.total_bytes) {
+    e = hipMalloc((void**)&c->d_ws, P.total_bytes);
+    if (e != hipSuccess)
+      return cleanup(fail(PRM_ENOMEM, "hipMalloc of %llu workspace bytes failed: %s",
+                          (unsigned long long)P.total_bytes, hipGetErrorString(e)));
+    e = hipMemsetAsync(c->d_ws, 0, P.total_bytes, c->stream);
+    if (e != hipSuccess) return cleanup(fail(PRM_EHIP, "hipMemsetAsync failed: %s", hipGetErrorString(e)));
+  }
+  const size_t nd = std::max<int32_t>(P.n, 1);
+  if ((e = hipMalloc((void**)&c->d_desc, sizeof(MatDesc) * nd)) != hipSuccess ||
+      (e = hipHostMalloc((void**)&c->h_desc, sizeof(MatDesc) * nd, hipHostMallocDefault)) != hipSuccess ||
+      (e = hipMalloc((void**)&c->d_ints, sizeof(int32_t) * P.ints.size())) != hipSuccess ||
+      (e = hipMalloc((void**)&c->d_items, sizeof(Item) * P.items.size())) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&c->upload_done, hipEventDisableTiming)) != hipSuccess)
+    return cleanup(fail(PRM_ENOMEM, "allocation failed: %s", hipGetErrorString(e)));
+  e = hipMemcpy(c->d_ints, P.ints.data(), sizeof(int32_t) * P.ints.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(c->d_items, P.items.data(), sizeof(Item) * P.items.size(), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return cleanup(fail(PRM_EHIP, "hipMemcpy failed: %s", hipGetErrorString(e)));
+  // static descriptor fields
+  c->desc.assign(P.n, MatDesc{});
+  c->last_ptrs.assign(4 * (size_t)P.n, nullptr);
+  char* chunk_base = c->d_ws;
+  char* small_base = c->d_ws + align256(P.chunk_bytes);
+  char* tall_base = small_base + P.small_bytes;
+  for (int i = 0; i < P.n; ++i) {
+    MatDesc& d = c->desc[i];
+    d.m = P.m[i];
+    d.n = P.nn[i];
+    d.s = P.s[i];
+    d.tall = P.tall[i];
+    d.rp = P.rp[i];
+    d.cp = P.cp[i];
+    const uint64_t xs = align256((uint64_t)d.rp * d.cp * 2), gs = align256((uint64_t)d.rp * d.rp * 2),
+                   vs = align256((uint64_t)d.rp * 4);
+    char* w = chunk_base + P.ws_off[i];
+    d.X = (uint16_t*)w;
+    d.XT = (uint16_t*)(w + xs);
+    d.Xn = (uint16_t*)(w + 2 * xs);
+    d.XTn = (uint16_t*)(w + 3 * xs);
+    d.Ao = (uint16_t*)(w + 4 * xs);
+    d.Bo = (uint16_t*)(w + 4 * xs + gs);
+    d.dA = (float*)(w + 4 * xs + 2 * gs);
+    d.dB = (float*)(w + 4 * xs + 2 * gs + vs);
+    d.ptiles_m = (int32_t)((d.tall ? d.cp : d.rp) / kPrologueTile);
+    d.ptiles_n = (int32_t)((d.tall ? d.rp : d.cp) / kPrologueTile);
+    d.partial = (float*)(small_base + P.small_off[i]);
+    d.alpha = d.partial + (int64_t)d.ptiles_m * d.ptiles_n;
+    if (d.tall) {
+      d.nrb = P.nrb[i];
+      d.colpart = (float*)(tall_base + P.tall_off[i]);
+      d.colinv = d.colpart + (int64_t)d.nrb * d.n;
+    }
+  }
+  e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return cleanup(fail(PRM_EHIP, "hipStreamSynchronize failed: %s", hipGetErrorString(e)));
+  *out = c;
+  return PRM_OK;
+}
+
+int prm_step(prm_ctx* ctx, void* const* params, const void* const* grads, float* const* momentum,
+             int64_t step, float lr, int32_t* did_refresh) {
+  return do_step(ctx, params, grads, momentum, step, lr, did_refresh, nullptr, false);
+}
+
+int prm_step_debug(prm_ctx* ctx, void* const* params, const void* const* grads,
+                   float* const* momentum, int64_t step, float lr, int32_t* did_refresh,
+                   float* const* direction_out) {
+  return do_step(ctx, params, grads, momentum, step, lr, did_refresh, direction_out, true);
+}
+
+int prm_profile_enable(prm_ctx* ctx, int32_t enable) {
+  if (!ctx) return fail(PRM_EINVAL, "ctx is NULL");
+  ctx->prof = enable != 0;
+  return PRM_OK;
+}
+
+int prm_profile_read(prm_ctx* ctx, prm_kernel_stats* out, int32_t n) {
+  if (!ctx) return fail(PRM_EINVAL, "ctx is NULL");
+  if (n > 0 && !out) return fail(PRM_EINVAL, "out is NULL");
+  HIP_TRY(hipStreamSynchronize(ctx->stream));
+  prm_kernel_stats acc[K_NCLASS];
+  std::memset(acc, 0, sizeof(acc));
+  for (int k = 0; k < K_NCLASS; ++k) std::snprintf(acc[k].name, sizeof(acc[k].name), "%s", kClassName[k]);
+  for (const auto& r : ctx->recs) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, r.e0, r.e1));
+    acc[r.cls].launches += 1;
+    acc[r.cls].total_ms += ms;
+    acc[r.cls].alg_bytes += r.bytes;
+    acc[r.cls].alg_flops += r.flops;
+  }
+  ctx->recs.clear();
+  ctx->pool_used = 0;
+  for (int k = 0; k < std::min<int32_t>(n, K_NCLASS); ++k) out[k] = acc[k];
+  return PRM_OK;
+}
+
+int prm_destroy(prm_ctx* c) {
+  if (!c) return PRM_OK;
+  int rc = PRM_OK;
+  if (c->d_ws || c->d_desc) {
+    if (hipStreamSynchronize(c->stream) != hipSuccess) rc = fail(PRM_EHIP, "hipStreamSynchronize failed in prm_destroy");
+  }
+  if (c->d_ws) (void)hipFree(c->d_ws);
+  if (c->d_desc) (void)hipFree(c->d_desc);
+  if (c->h_desc) (void)hipHostFree(c->h_desc);
+  if (c->d_ints) (void)hipFree(c->d_ints);
+  if (c->d_items) (void)hipFree(c->d_items);
+  if (c->upload_done) (void)hipEventDestroy(c->upload_done);
+  for (auto e : c->pool) (void)hipEventDestroy(e);
+  delete c;
+  return rc;
+}
+
+const char* prm_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// Device helpers shared by the libprm kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "prm_internal.h"
+
+namespace prm {
+
+// ---- bf16 <-> fp32 ---------------------------------------------------------
+__device__ __forceinline__ float bf2f(uint32_t h) { return __uint_as_float(h << 16); }
+
+// Round to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ uint32_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
+  return f2bf(lo) | (f2bf(hi) << 16);
+}
+
+// ---- typed loads / stores of 4 or 8 consecutive elements --------------------
+// Element storage type T is either float or uint16_t (bf16 bits).
+template <typename T> struct Vec;
+
+template <> struct Vec<float> {
+  __device__ __forceinline__ static void load4(const float* p, float v[4]) {
+    float4 x = *reinterpret_cast<const float4*>(p);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  }
+  __device__ __forceinline__ static void store4(float* p, const float v[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  __device__ __forceinline__ static void load8(const float* p, float v[8]) {
+    load4(p, v);
+    load4(p + 4, v + 4);
+  }
+  __device__ __forceinline__ static void store8(float* p, const float v[8]) {
+    store4(p, v);
+    store4(p + 4, v + 4);
+  }
+  __device__ __forceinline__ static float load1(const float* p) { return *p; }
+  __device__ __forceinline__ static void store1(float* p, float v) { *p = v; }
+};
+
+template <> struct Vec<uint16_t> {
+  __device__ __forceinline__ static void load4(const uint16_t* p, float v[4]) {
+    uint2 x = *reinterpret_cast<const uint2*>(p);
+    v[0] = bf2f(x.x & 0xffffu); v[1] = bf2f(x.x >> 16);
+    v[2] = bf2f(x.y & 0xffffu); v[3] = bf2f(x.y >> 16);
+  }
+  __device__ __forceinline__ static void store4(uint16_t* p, const float v[4]) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+  }
+  __device__ __forceinline__ static void load8(const uint16_t* p, float v[8]) {
+    uint4 x = *reinterpret_cast<const uint4*>(p);
+    v[0] = bf2f(x.x & 0xffffu); v[1] = bf2f(x.x >> 16);
+    v[2] = bf2f(x.y & 0xffffu); v[3] = bf2f(x.y >> 16);
+    v[4] = bf2f(x.z & 0xffffu); v[5] = bf2f(x.z >> 16);
+    v[6] = bf2f(x.w & 0xffffu); v[7] = bf2f(x.w >> 16);
+  }
+  __device__ __forceinline__ static void store8(uint16_t* p, const float v[8]) {
+    *reinterpret_cast<uint4*>(p) = make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]),
+                                              pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7]));
+  }
+  __device__ __forceinline__ static float load1(const uint16_t* p) { return bf2f(*p); }
+  __device__ __forceinline__ static void store1(uint16_t* p, float v) { *p = (uint16_t)f2bf(v); }
+};
+
+// ---- reductions (fixed order: deterministic run to run) ---------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sum over a whole workgroup of NT threads (NT a multiple of 64, <= 1024).
+// `red` must hold NT/64 floats.  Every thread gets the total.
+template <int NT>
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  if constexpr (NT == 64) {
+    return v;
+  } else {
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[w] = v;
+    __syncthreads();
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < NT / 64; ++i) t += red[i];
+    return t;
+  }
+}
+
+// Binary search: index of the last segment whose start <= b.
+__device__ __forceinline__ int find_segment(const int32_t* start, int n, int b) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (start[mid] <= b) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+}  // namespace prm

@@ -1,0 +1,114 @@
+// Internal definitions of libprm: the per-matrix descriptor shared by the host
+// dispatcher and the gfx950 kernels, launch parameter blocks, and the
+// kernel-launch entry points that the dispatcher calls.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace prm {
+
+// One entry per matrix, in the order given to prm_init.  Caller pointers
+// (W, G, M, D) are refreshed before a step whenever they change; the rest is
+// fixed at prm_init.
+struct MatDesc {
+  // caller buffers (device, row-major m x n)
+  void* W;
+  const void* G;
+  float* M;
+  float* D;  // direction output (prm_step_debug) or nullptr
+  int64_t m, n;
+  float s;       // shape scale s(W)
+  int32_t tall;  // m > n: oriented rows are stored columns
+  // NS5 workspace (bf16 bit patterns), valid while this matrix's chunk runs.
+  // Oriented r x c is padded to rp x cp (multiples of the GEMM tile).
+  uint16_t* X;    // rp x cp   iterate, row-major
+  uint16_t* XT;   // cp x rp   its transpose
+  uint16_t* Xn;   // rp x cp   next iterate
+  uint16_t* XTn;  // cp x rp
+  uint16_t* Ao;   // rp x rp   Gram matrix A = X X^T with its diagonal set to zero (bf16)
+  uint16_t* Bo;   // rp x rp   B = b A + c A^2 with its diagonal set to zero (bf16)
+  float* dA;      // rp        diagonal of A (fp32)
+  float* dB;      // rp        diagonal of B (fp32)
+  float* partial; // prologue: one sum of squares per 64 x 64 tile
+  float* alpha;   // 1 / (||U||_F + eps_ns)
+  int64_t rp, cp;
+  int32_t ptiles_m, ptiles_n;  // prologue tile grid over the padded stored shape
+  // row-wise tall path
+  float* colpart;  // [nrb][n] partial column sums of squares
+  float* colinv;   // [n] 1 / max(||column||, eps)
+  int32_t nrb;     // row blocks of the tall statistics pass
+  int32_t pad0;
+};
+
+// Per-launch scalars of the row-wise kernels.
+struct RwParams {
+  float beta;      // momentum coefficient
+  float gcoef;     // 1 (heavy-ball) or 1 - beta (dampening)
+  float lr;        // eta_t
+  float decay;     // 1 - eta_t * lambda
+  float gamma;     // RowNorm multiplier
+  float eps;       // RowNorm clamp
+  int32_t nesterov;
+  int32_t write_d;
+};
+
+// Per-launch scalars of the NS5 kernels.
+struct NsParams {
+  float beta, gcoef;
+  int32_t nesterov;
+  float eps_ns;
+  float a, b, c;    // quintic coefficients
+  float lr, decay;
+  float dscale;     // 1, or gamma for the scalar-controlled ablation
+  int32_t iter;     // 0 .. 4
+  int32_t last;     // iter == NS iterations - 1
+  int32_t write_d;
+};
+
+// Work item of the tiled kernels.
+struct Item {
+  int32_t mat;
+  int32_t tm;   // tile row (or row block)
+  int32_t tn;   // tile column (or column slab)
+  int32_t aux;
+};
+
+enum DType : int32_t { F32 = 0, BF16 = 1 };
+
+// ---- launchers (defined in rowwise.hip / ns5.hip) -------------------------
+// Wide/square matrices, whole rows held in registers.  seg_start[i] is the
+// first block of segment i (matrix seg_mat[i]); nblocks blocks in total.
+hipError_t launch_rw_wide(int tpr, int nch, DType wt, DType gt, const MatDesc* md,
+                          const int32_t* seg_mat, const int32_t* seg_start, int32_t nseg,
+                          int32_t nblocks, const RwParams& p, hipStream_t s);
+// Any shape (unaligned rows, very long rows): two sweeps over the row.
+hipError_t launch_rw_generic(DType wt, DType gt, const MatDesc* md, const int32_t* rows_mat,
+                             const int32_t* rows_start, int32_t nseg, int32_t nrows_total,
+                             const RwParams& p, hipStream_t s);
+// Tall matrices: column statistics, column norms, parameter write.
+hipError_t launch_rw_tall_stats(int vec, DType gt, const MatDesc* md, const Item* items,
+                                int32_t nitems, const RwParams& p, hipStream_t s);
+hipError_t launch_rw_tall_finalize(const MatDesc* md, const Item* items, int32_t nitems,
+                                   const RwParams& p, hipStream_t s);
+hipError_t launch_rw_tall_apply(int vec, DType wt, DType gt, const MatDesc* md,
+                                const Item* items, int32_t nitems, const RwParams& p,
+                                hipStream_t s);
+
+// NS5 refresh.
+hipError_t launch_ns_prologue(DType gt, const MatDesc* md, const Item* items, int32_t nitems,
+                              const NsParams& p, hipStream_t s);
+hipError_t launch_ns_alpha(const MatDesc* md, const int32_t* mats, int32_t nmats,
+                           const NsParams& p, hipStream_t s);
+enum GemmKind : int32_t { GEMM_GRAM = 0, GEMM_POLY = 1, GEMM_APPLY = 2 };
+hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item* items,
+                          int32_t nitems, const NsParams& p, hipStream_t s);
+
+// GEMM tile edge used by the NS5 kernels; rp and cp are multiples of it.
+constexpr int kNsTile = 128;
+// Prologue tile edge.
+constexpr int kPrologueTile = 64;
+// Row block of the tall statistics pass.
+constexpr int kTallRows = 128;
+
+}  // namespace prm

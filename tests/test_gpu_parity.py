@@ -1,0 +1,226 @@
+"""GPU parity: libprm (through the C ABI) against the fp64 oracle on the same
+seeded inputs, at sizes the oracle finishes in seconds.  Shapes are chosen to
+reach every launch path: wide rows held in registers with 64 / 256 / 512
+threads per row, the generic wide path (unaligned or very long rows), the
+tall two-pass path with 4-wide and scalar columns, NS5 with padded tiles,
+multiple tiles, several workspace chunks, and degenerate 1 x 1, 1 x n and
+m x 1 matrices."""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import paper_2608_20818_amd as prm  # noqa: E402
+import prm_case as pc  # noqa: E402
+import synth  # noqa: E402
+from oracle import prm_oracle as po  # noqa: E402
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+RAGGED = [(256, 768), (130, 130), (200, 4104), (40, 17000), (37, 333), (3, 33000),
+          (520, 136), (301, 77), (1, 1), (1, 64), (64, 1), (384, 1280), (1024, 256)]
+
+
+def run_one_step(shapes, cfg, t, workload_id=90, inputs=None):
+    """One prm_step_debug at step t on fresh seeded inputs; returns GPU and
+    oracle results as float64 host arrays."""
+    inputs = inputs or pc.host_inputs(shapes, cfg, workload_id, steps=(t,))
+    dev = "cuda"
+    W = [pc.to_device(w, cfg.param_dtype) for w, _, _ in inputs]
+    M = [pc.to_device(m, 0) for _, m, _ in inputs]
+    G = [pc.to_device(g[t], cfg.grad_dtype) for _, _, g in inputs]
+    D = [torch.zeros(s, dtype=torch.float32, device=dev) for s in shapes]
+    with prm.Optimizer(shapes, cfg) as opt:
+        rho = opt.step(W, G, M, t, directions=D)
+        torch.cuda.synchronize()
+    oc = pc.oracle_config(cfg)
+    res = []
+    for i, (w0, m0, g) in enumerate(inputs):
+        Wo, Mo, Do, rho_o = po.step_matrix(w0, m0, g[t], t, oc)
+        res.append(dict(W=pc.to_host(W[i]), M=pc.to_host(M[i]), D=pc.to_host(D[i]),
+                        Wo=Wo, Mo=Mo, Do=Do, W0=w0))
+        assert rho == rho_o
+    return rho, res
+
+
+def check(res, rho, cfg, shapes, lr):
+    tol = pc.TOL_NS5 if rho else pc.TOL_ROWWISE
+    for (m, n), r in zip(shapes, res):
+        eD = pc.rel(r["D"], r["Do"])
+        eM = pc.rel(r["M"], r["Mo"])
+        print(f"  {m}x{n} rho={rho} D_err={eD:.3e} M_err={eM:.3e}", flush=True)
+        assert eD <= tol, f"{m}x{n} rho={rho}: D rel err {eD:.3e} > {tol}"
+        assert eM <= pc.TOL_M, f"{m}x{n}: M rel err {eM:.3e}"
+        if cfg.param_dtype == prm.F32:
+            # W_gpu - W_oracle = -eta (D_gpu - D_oracle) up to fp32 rounding
+            bound = pc.f32(lr) * np.linalg.norm(r["D"] - r["Do"]) * 1.01 + 4e-7 * np.linalg.norm(r["Wo"]) + 1e-30
+            assert np.linalg.norm(r["W"] - r["Wo"]) <= bound, f"{m}x{n}: W"
+        else:
+            # W_gpu = bf16(decay W0 - eta D_gpu): within half a bf16 ulp of the
+            # exact update with the GPU's own direction, which differs from the
+            # oracle's update by eta |D_gpu - D_oracle|
+            slack = pc.bf16_write_bound(r["W"], r["Wo"], r["D"], r["Do"], lr)
+            assert slack <= 1.0, f"{m}x{n}: W outside the rounding bound ({slack:.3f})"
+
+
+@pytest.mark.parametrize("t", [0, 1])
+@pytest.mark.parametrize("wdt,gdt", [(1, 1), (0, 0), (1, 0), (0, 1)])
+def test_ragged_shapes_all_paths(t, wdt, gdt):
+    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=wdt, grad_dtype=gdt)
+    rho, res = run_one_step(RAGGED, cfg, t)
+    assert rho == (1 if t == 0 else 0)
+    check(res, rho, cfg, RAGGED, cfg.lr)
+
+
+@pytest.mark.parametrize("flag", ["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh"])
+@pytest.mark.parametrize("t", [0, 3])
+def test_variants(flag, t):
+    shapes = [(96, 320), (300, 88), (64, 64), (33, 130)]
+    cfg = prm.config_default(K=3, lr=0.01, wd=0.05, param_dtype=0, grad_dtype=1, **{flag: 1})
+    rho, res = run_one_step(shapes, cfg, t, workload_id=91)
+    assert rho == (0 if flag == "never_refresh" else 1)
+    check(res, rho, cfg, shapes, cfg.lr)
+
+
+def test_several_workspace_chunks():
+    shapes = [(256, 512), (512, 256), (128, 640), (200, 200), (256, 512)]
+    one = 8 * 256 * 640 + 6 * 256 * 256 + 4096
+    cfg = prm.config_default(K=2, lr=0.01, wd=0.01, workspace_budget_bytes=one)
+    assert prm.workspace_bytes(shapes, cfg) < prm.workspace_bytes(shapes, prm.config_default())
+    rho, res = run_one_step(shapes, cfg, 0, workload_id=92)
+    check(res, rho, cfg, shapes, cfg.lr)
+
+
+def test_zero_and_tiny_rows_rownorm_eps():
+    # eq. (rownorm): a zero oriented row gives a zero direction, a row whose
+    # norm is below eps is divided by eps.
+    shapes = [(6, 40), (48, 5)]
+    cfg = prm.config_default(K=5, lr=0.1, wd=0.0, param_dtype=0, grad_dtype=0, beta=0.0,
+                             eps_rownorm=1e-3)
+    rng = np.random.default_rng(3)
+    inputs = []
+    for (m, n) in shapes:
+        G = rng.standard_normal((m, n)).astype(np.float32).astype(np.float64)
+        if m <= n:
+            G[1] = 0.0
+            G[2] = 1e-5
+        else:
+            G[:, 1] = 0.0
+            G[:, 2] = 1e-5
+        inputs.append((np.ones((m, n)), np.zeros((m, n)), {1: G}))
+    rho, res = run_one_step(shapes, cfg, 1, inputs=inputs)
+    assert rho == 0
+    check(res, rho, cfg, shapes, cfg.lr)
+    r0 = res[0]
+    np.testing.assert_array_equal(r0["D"][1], 0.0)
+    np.testing.assert_allclose(r0["D"][2], 0.15 * 1e-5 / pc.f32(1e-3), rtol=1e-5)
+
+
+def test_zero_momentum_refresh_gives_pure_decay():
+    shapes = [(64, 192), (192, 64)]
+    cfg = prm.config_default(K=1, lr=0.5, wd=0.1, param_dtype=0, grad_dtype=0)
+    inputs = [(np.full((m, n), 0.25), np.zeros((m, n)), {0: np.zeros((m, n))}) for m, n in shapes]
+    rho, res = run_one_step(shapes, cfg, 0, inputs=inputs)
+    assert rho == 1
+    for r in res:
+        np.testing.assert_array_equal(r["D"], 0.0)
+        np.testing.assert_allclose(r["W"], np.float32(0.25) * np.float32(1 - np.float32(0.5) * np.float32(0.1)))
+
+
+def test_tiny_workload_trajectory():
+    """The tiny workload: 6 fp32 matrices, K = 4, eight steps t = 0..7 (two
+    refreshes), lr 0.02, wd 0.1; every step compared with the oracle's own
+    trajectory from the same initial state and gradients."""
+    wl = synth.WORKLOADS[0]
+    shapes = list(wl.shapes)
+    cfg = prm.config_default(K=wl.K, lr=wl.lr, wd=wl.wd, param_dtype=0, grad_dtype=0)
+    steps = range(8)
+    inputs = synth.host_workload(0, steps=steps)
+    W = [pc.to_device(w, 0) for w, _, _ in inputs]
+    M = [pc.to_device(m, 0) for _, m, _ in inputs]
+    D = [torch.zeros(s, dtype=torch.float32, device="cuda") for s in shapes]
+    Wo = [w for w, _, _ in inputs]
+    Mo = [m for _, m, _ in inputs]
+    oc = pc.oracle_config(cfg)
+    with prm.Optimizer(shapes, cfg) as opt:
+        werr_budget = np.zeros(len(shapes))
+        for t in steps:
+            G = [pc.to_device(g[t], 0) for _, _, g in inputs]
+            rho = opt.step(W, G, M, t, directions=D)
+            torch.cuda.synchronize()
+            Wo, Mo, Do, rho_o = po.step(Wo, Mo, [g[t] for _, _, g in inputs], t, oc)
+            assert rho == rho_o == (1 if t % 4 == 0 else 0)
+            tol = pc.TOL_NS5 if rho else pc.TOL_ROWWISE
+            for i in range(len(shapes)):
+                d = pc.to_host(D[i])
+                eD = pc.rel(d, Do[i])
+                assert eD <= tol, f"t={t} mat {i} {shapes[i]}: D err {eD:.3e}"
+                assert pc.rel(pc.to_host(M[i]), Mo[i]) <= pc.TOL_M
+                werr_budget[i] += pc.f32(cfg.lr) * np.linalg.norm(d - Do[i]) * 1.01
+                werr = np.linalg.norm(pc.to_host(W[i]) - Wo[i])
+                assert werr <= werr_budget[i] + 1e-6 * np.linalg.norm(Wo[i]), f"t={t} mat {i}: W"
+
+
+def _state(shapes, cfg, seed):
+    inputs = pc.host_inputs(shapes, cfg, seed, steps=range(8))
+    W = [pc.to_device(w, cfg.param_dtype) for w, _, _ in inputs]
+    M = [pc.to_device(m, 0) for _, m, _ in inputs]
+    Gs = {t: [pc.to_device(g[t], cfg.grad_dtype) for _, _, g in inputs] for t in range(8)}
+    return W, M, Gs
+
+
+def test_bitwise_deterministic_and_resumable():
+    shapes = [(130, 390), (390, 130), (64, 64), (8, 4104)]
+    cfg = prm.config_default(K=3, lr=0.01)
+    W1, M1, Gs = _state(shapes, cfg, 93)
+    W2, M2, _ = _state(shapes, cfg, 93)
+    with prm.Optimizer(shapes, cfg) as opt:
+        for t in range(8):
+            opt.step(W1, Gs[t], M1, t)
+    # same trajectory in two contexts: 4 steps, destroy, re-init, 4 more
+    with prm.Optimizer(shapes, cfg) as opt:
+        for t in range(4):
+            opt.step(W2, Gs[t], M2, t)
+    torch.cuda.synchronize()
+    with prm.Optimizer(shapes, cfg) as opt:
+        for t in range(4, 8):
+            opt.step(W2, Gs[t], M2, t)
+    torch.cuda.synchronize()
+    for a, b in zip(W1 + M1, W2 + M2):
+        assert torch.equal(a, b)
+
+
+def test_empty_matrix_list_and_pointer_changes():
+    cfg = prm.config_default()
+    with prm.Optimizer([], cfg) as opt:
+        assert opt.step([], [], [], 0) == 1
+        assert opt.step([], [], [], 1) == 0
+    # new tensors every call: the pointer table is re-uploaded
+    shapes = [(16, 48)]
+    with prm.Optimizer(shapes, cfg) as opt:
+        for t in range(4):
+            W, M, Gs = _state(shapes, cfg, 94)
+            opt.step(W, Gs[t], M, t)
+    torch.cuda.synchronize()
+
+
+def test_misaligned_pointer_rejected_without_side_effects():
+    shapes = [(8, 16)]
+    cfg = prm.config_default(param_dtype=0, grad_dtype=0)
+    base = torch.zeros(8 * 16 + 4, dtype=torch.float32, device="cuda")
+    W = base[1:1 + 128].view(8, 16)
+    G = torch.ones(8, 16, device="cuda")
+    M = torch.ones(8, 16, device="cuda")
+    with prm.Optimizer(shapes, cfg) as opt:
+        with pytest.raises(prm.PRMError) as e:
+            opt.step([W], [G], [M], 0)
+        assert e.value.code == prm.PRM_EALIGN
+        with pytest.raises(prm.PRMError) as e:
+            opt.step([G], [G], [M], -1)
+        assert e.value.code == prm.PRM_EINVAL
+    torch.cuda.synchronize()
+    assert torch.equal(M, torch.ones_like(M))
