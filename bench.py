@@ -1,0 +1,308 @@
+#!/usr/bin/env python3
+"""Benchmark of the Periodic Row-wise Muon optimizer step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps S] [--warmup W] [--config 2] [--K K]
+
+A "step" is one optimizer step t of the whole hot path over every matrix of a
+synthetic DiT-shaped weight set (inputs resident in HBM): momentum update, then
+NS5 refresh when t mod K = 0, else the row-wise RowNorm step, then the
+parameter write.  Warmup runs steps t = 0..W-1; the timed window runs
+t = W..W+S-1 (with the defaults it starts at a refresh and covers two whole
+periods).  ``value`` is the amortized optimizer time per step over a period,
+(T_refresh + (K-1) T_rowwise) / K, from HIP events on the library's stream.
+
+After the timed window one more period runs with per-kernel HIP events
+(libprm's profiling hooks) to attribute time to kernels; the dominant kernel's
+algorithmic FLOPs (or bytes) per launch over its mean launch time give the
+``roofline`` object.  The oracle (fp64 NumPy) is timed on a bounded sample of
+the same workload on the host cores and extrapolated (``cpu_baseline``).
+
+Only rank 0 at N = 1 runs; there is no multi-GPU path.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = ("optimizer ms/step (NS5 refresh, row-wise, amortized over K) at DiT-4B; MFMA%/HBM%")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 2K)")
+    ap.add_argument("--warmup", type=int, default=None, help="warmup steps (default K)")
+    ap.add_argument("--config", type=int, default=2,
+                    help="workload index: 0 tiny, 1 DiT-1.3B, 2 DiT-4B (default), 3 DiT-9B, 4 DiT-15B")
+    ap.add_argument("--K", type=int, default=None, help="refresh period (default: the workload's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel attribution period")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a 4 GiB device-to-device copy (HBM bandwidth and counter calibration)")
+    return ap.parse_args()
+
+
+def copy_probe():
+    import torch
+    n = 1 << 30  # fp32 elements: 4 GiB read + 4 GiB written per copy
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(2):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    reps = 10
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    gbs = 2 * 4 * n / ms / 1e6
+    print(json.dumps({"copy_probe": {"bytes_read": 4 * n, "bytes_written": 4 * n, "ms": ms,
+                                     "GB_s": gbs, "frac_of_spec": gbs / PEAK_HBM_GBS}}), flush=True)
+
+
+def make_inputs(wl_idx, wl, device):
+    import torch
+    import synth
+    W, M, G = [], [], []
+    t0 = time.time()
+    for i, (m, n) in enumerate(wl.shapes):
+        d = synth.device_matrix(wl_idx, i, m, n, synth.rank_of(wl, m, n), param_dtype=wl.param_dtype,
+                                grad_dtype=wl.grad_dtype, device=device, beta=wl.beta, step=0)
+        W.append(d["W"])
+        M.append(d["M"])
+        G.append(d["G"])
+        if i % 40 == 39:
+            torch.cuda.synchronize()
+            log(f"[bench] inputs {i + 1}/{len(wl.shapes)} ({time.time() - t0:.1f}s)")
+    torch.cuda.synchronize()
+    return W, M, G
+
+
+def cpu_baseline(wl_idx, wl, K, cfg_vals):
+    """Time the fp64 oracle on a bounded sample of the workload and scale it to
+    one optimizer step of the whole weight set."""
+    import numpy as np
+    import synth
+    from oracle import prm_oracle as po
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        threads = max((p.get("num_threads", 1) for p in blas), default=1)
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threads = os.cpu_count() or 1
+    oc = po.PRMConfig(K=K, **cfg_vals)
+    shapes = wl.shapes
+    # NS5 sample: the matrix with the fewest NS5 FLOPs (cheapest representative)
+    flops = [po.ns5_flops(m, n) for m, n in shapes]
+    i_ns = min(range(len(shapes)), key=lambda i: flops[i])
+    # row-wise sample: 256 full oriented rows of the longest wide matrix and of a
+    # tall matrix (the oracle's per-element cost does not depend on the row count)
+    i_wide = max((i for i, (m, n) in enumerate(shapes) if m <= n), key=lambda i: shapes[i][1])
+    i_tall = next((i for i, (m, n) in enumerate(shapes) if m > n), None)
+    rw_shapes = [(min(256, shapes[i_wide][0]), shapes[i_wide][1])]
+    if i_tall is not None:
+        rw_shapes.append((shapes[i_tall][0], min(256, shapes[i_tall][1])))
+    m, n = shapes[i_ns]
+    w, mm, g = synth.host_matrix(wl_idx, i_ns, m, n, synth.rank_of(wl, m, n), param_dtype=wl.param_dtype,
+                                 grad_dtype=wl.grad_dtype, beta=wl.beta, steps=(0,))
+    t0 = time.perf_counter()
+    po.step_matrix(w, mm, g[0], 0, oc)
+    t_ns = time.perf_counter() - t0
+    rw_elems, t_rw = 0, 0.0
+    for j, (m, n) in enumerate(rw_shapes):
+        w, mm, g = synth.host_matrix(wl_idx, 10_000 + j, m, n, synth.rank_of(wl, m, n),
+                                     param_dtype=wl.param_dtype, grad_dtype=wl.grad_dtype,
+                                     beta=wl.beta, steps=(1,))
+        t0 = time.perf_counter()
+        po.step_matrix(w, mm, g[1], 1, oc)
+        t_rw += time.perf_counter() - t0
+        rw_elems += m * n
+    total_flops = sum(flops)
+    total_elems = sum(m * n for m, n in shapes)
+    T_ref = t_ns * total_flops / flops[i_ns] * 1e3
+    T_rw = t_rw / rw_elems * total_elems * 1e3
+    amort = (T_ref + (K - 1) * T_rw) / K
+    return {
+        "value": amort, "unit": "ms", "cores": int(threads), "kind": "oracle",
+        "host_cpus": os.cpu_count(),
+        "refresh_ms": T_ref, "rowwise_ms": T_rw,
+        "sample": (f"fp64 NumPy oracle: one refresh step of matrix {shapes[i_ns]} ({t_ns:.1f}s) scaled by "
+                   f"NS5 FLOPs (x{total_flops / flops[i_ns]:.1f}); one row-wise step of "
+                   f"{' and '.join(str(s) for s in rw_shapes)} (full oriented rows, {t_rw:.2f}s) scaled "
+                   f"by elements (x{total_elems / rw_elems:.1f}); amortized over K={K}"),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}, WORLD_SIZE "
+              f"{world}); the multi-GPU sharding is a design note, not an implemented path.",
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+    import torch
+
+    if args.copy_probe:
+        copy_probe()
+        return
+    import paper_2608_20818_amd as prm
+    import synth
+    from oracle import prm_oracle as po
+
+    wl = synth.WORKLOADS[args.config]
+    K = args.K or wl.K
+    steps = args.steps if args.steps is not None else 2 * K
+    warmup = args.warmup if args.warmup is not None else K
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    shapes = list(wl.shapes)
+    dt = {"f32": prm.F32, "bf16": prm.BF16}
+    cfg = prm.config_default(K=K, lr=wl.lr, wd=wl.wd, gamma=wl.gamma, beta=wl.beta,
+                             param_dtype=dt[wl.param_dtype], grad_dtype=dt[wl.grad_dtype])
+    log(f"[bench] workload {wl.name}: {len(shapes)} matrices, "
+        f"{sum(m * n for m, n in shapes) / 1e9:.3f} G elements, K={K}, steps={steps}, warmup={warmup}")
+    W, M, G = make_inputs(args.config, wl, dev)
+    log(f"[bench] inputs ready; workspace {prm.workspace_bytes(shapes, cfg) / 2**30:.1f} GiB")
+
+    stream = torch.cuda.current_stream()
+    opt = prm.Optimizer(shapes, cfg, stream=stream.cuda_stream)
+    t = 0
+    for _ in range(warmup):
+        opt.step(W, G, M, t)
+        t += 1
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    kinds = []
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(steps):
+        evs[i][0].record(stream)
+        kinds.append(opt.step(W, G, M, t))
+        evs[i][1].record(stream)
+        t += 1
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3
+    per = [a.elapsed_time(b) for a, b in evs]
+    ref = [x for x, k in zip(per, kinds) if k == 1]
+    rw = [x for x, k in zip(per, kinds) if k == 0]
+    T_ref = statistics.median(ref) if ref else float("nan")
+    T_rw = statistics.median(rw) if rw else float("nan")
+    if K == 1:
+        amort = T_ref
+    elif ref and rw:
+        amort = (T_ref + (K - 1) * T_rw) / K
+    else:
+        amort = sum(per) / len(per)
+    log(f"[bench] timed {steps} steps: refresh {T_ref:.2f} ms, row-wise {T_rw:.3f} ms, amortized {amort:.3f} ms")
+
+    # algorithmic work of one refresh and one row-wise step of the whole set
+    wb = 2 if wl.param_dtype == "bf16" else 4
+    gb = 2 if wl.grad_dtype == "bf16" else 4
+    elems = sum(m * n for m, n in shapes)
+    rw_bytes = elems * (gb + 4 + 4 + 2 * wb)
+    ns_flops = sum(po.ns5_flops(m, n) for m, n in shapes)
+    refresh_mfma_frac = ns_flops / (T_ref * 1e-3) / (PEAK_BF16_TFLOPS * 1e12) if ref else None
+    rowwise_hbm_frac = rw_bytes / (T_rw * 1e-3) / (PEAK_HBM_GBS * 1e9) if rw else None
+
+    kernels, roofline, roofline_rw = None, None, None
+    if not args.no_profile:
+        while t % K != 0:
+            t += 1
+        opt.profile_enable(True)
+        for _ in range(K):
+            opt.step(W, G, M, t)
+            t += 1
+        kernels = opt.profile_read()
+        opt.profile_enable(False)
+        dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
+        kd = kernels[dom]
+
+        def roof(name, k):
+            if k["launches"] == 0 or k["total_ms"] <= 0:
+                return None
+            mean_ms = k["total_ms"] / k["launches"]
+            if k["alg_flops"] > 0:
+                ach = k["alg_flops"] / k["launches"] / (mean_ms * 1e-3) / 1e12
+                return {"kernel": name, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
+                        "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": None,
+                        "launches": k["launches"], "mean_launch_ms": mean_ms,
+                        "alg_per_launch": k["alg_flops"] / k["launches"]}
+            ach = k["alg_bytes"] / k["launches"] / (mean_ms * 1e-3) / 1e9
+            return {"kernel": name, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
+                    "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None,
+                    "launches": k["launches"], "mean_launch_ms": mean_ms,
+                    "alg_per_launch": k["alg_bytes"] / k["launches"]}
+
+        roofline = roof(dom, kd)
+        rw_names = [k for k in ("rw_wide", "rw_generic", "rw_tall_stats", "rw_tall_apply") if kernels[k]["launches"]]
+        if rw_names:
+            dom_rw = max(rw_names, key=lambda k: kernels[k]["total_ms"])
+            roofline_rw = roof(dom_rw, kernels[dom_rw])
+        log(f"[bench] kernels: " + ", ".join(f"{k} {v['total_ms']:.2f}ms/{v['launches']}" for k, v in kernels.items() if v["launches"]))
+
+    opt.close()
+    cpu = None
+    if not args.no_cpu_baseline:
+        del W, M, G
+        torch.cuda.empty_cache()
+        log("[bench] timing the oracle on the host (bounded sample)")
+        cpu = cpu_baseline(args.config, wl, K, dict(beta=wl.beta, lr=wl.lr, wd=wl.wd, gamma=wl.gamma))
+
+    out = {
+        "metric": METRIC,
+        "value": amort,
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": wall_ms / steps,
+        "ms_per_step_events": sum(per) / len(per),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "dtype_detail": "NS5: bf16 MFMA inputs, fp32 accumulation; momentum, RowNorm and update: fp32; "
+                        f"W {wl.param_dtype}, G {wl.grad_dtype}, M f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "matrices": len(shapes), "elements": elems, "K": K,
+                   "lr": wl.lr, "wd": wl.wd, "gamma": wl.gamma, "beta": wl.beta,
+                   "param_dtype": wl.param_dtype, "grad_dtype": wl.grad_dtype, "momentum_dtype": "f32",
+                   "parallelism": "single GPU"},
+        "refresh_ms": T_ref,
+        "rowwise_ms": T_rw,
+        "refresh_mfma_frac": refresh_mfma_frac,
+        "rowwise_hbm_frac": rowwise_hbm_frac,
+        "refresh_alg_tflop": ns_flops / 1e12,
+        "rowwise_alg_gb": rw_bytes / 1e9,
+        "roofline": roofline,
+        "roofline_rowwise": roofline_rw,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+        "paper_context": "46.9-54.3% optimizer-time reduction of PRM (K=3) vs Muon on 256 H100 with "
+                         "FSDP2, normalized units, communication included",
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
