@@ -14,7 +14,7 @@
 //    (alpha^2) and the first apply (alpha) epilogues.
 //  * ns_alpha: fixed-order reduction of the tile sums into alpha.
 //  * ns_gemm: C = P Q^T on bf16 operands with fp32 MFMA accumulation
-//    (v_mfma_f32_32x32x16_bf16), 128 x 128 tiles, BK = 64, LDS double buffer
+//    (v_mfma_f32_32x32x16_bf16), 256 x 256 tiles, BK = 64, LDS double buffer
 //    with an XOR swizzle.  Every product of the iteration has this NT form:
 //      Gram   A   = X X^T              (upper tiles only, mirrored)
 //      square A^2 = A A^T              (A is symmetric; upper tiles, mirrored)
@@ -127,6 +127,12 @@ __global__ __launch_bounds__(256) void ns_alpha_kernel(const MatDesc* __restrict
 
 // ---------------------------------------------------------------------------
 // batched NT GEMM with fused NS5 epilogues
+//
+// Work-group tile 256 x 256, four waves in a 2 x 2 grid, each wave owning a
+// 128 x 128 block as 4 x 4 MFMA 32x32x16 accumulators (256 fp32 per lane).
+// K advances in stages of 64: global loads of stage k+1 are issued into
+// registers before stage k is computed from LDS, then written to the other
+// LDS buffer.  Per stage and wave: 64 MFMAs against 32 fragment reads.
 // ---------------------------------------------------------------------------
 namespace gemm {
 constexpr int BM = kNsTile, BN = kNsTile, BK = 64;
@@ -134,19 +140,44 @@ constexpr int NTHREADS = 256;
 constexpr int WM = BM / 2, WN = BN / 2;  // 2 x 2 waves
 constexpr int MI = WM / 32, NI = WN / 32;
 constexpr int ROW_BYTES = BK * 2;                       // 128 B per tile row
-constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;      // 32 KB
-constexpr int OP_BYTES = 2 * STAGE_BYTES;               // 64 KB
-constexpr int EPI_LD = BN + 4;                          // fp32 words per staged row
-constexpr int EPI_BYTES = BM * EPI_LD * 4;              // 66 KB
+constexpr int A_BYTES = BM * ROW_BYTES;                 // 32 KB
+constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;      // 64 KB
+constexpr int OP_BYTES = 2 * STAGE_BYTES;               // 128 KB
+constexpr int HM = BM / 2;                              // epilogue works on half tiles
+constexpr int EPI_LD = BN + 8;                          // fp32 words per staged row
+constexpr int EPI_BYTES = HM * EPI_LD * 4;              // 132 KB
 constexpr int LDS_BYTES = OP_BYTES > EPI_BYTES ? OP_BYTES : EPI_BYTES;
 constexpr int LOADS = BM * (BK / 8) / NTHREADS;         // 16-byte chunks per thread per operand
 
 // byte offset of 16-byte chunk `ch` of tile row `r` (XOR swizzle over 8 chunks)
 __device__ __forceinline__ int swz(int r, int ch) { return r * ROW_BYTES + ((ch ^ (r & 7)) << 4); }
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(1))) u32x4* gptr4;
+
+// One stage of both operands into registers: chunk i of this thread is tile
+// row (thread/8 + 32 i), 16-byte chunk thread%8, at uint4 offset `ko` along K.
+__device__ __forceinline__ void stage_load(u32x4 (&ra)[LOADS], u32x4 (&rb)[LOADS], gptr4 pa,
+                                           gptr4 pb, int64_t rstep, int64_t ko) {
+#pragma unroll
+  for (int i = 0; i < LOADS; ++i) {
+    ra[i] = pa[i * rstep + ko];
+    rb[i] = pb[i * rstep + ko];
+  }
+}
+
+__device__ __forceinline__ void stage_store(char* stage, const u32x4 (&ra)[LOADS],
+                                            const u32x4 (&rb)[LOADS], const int (&soff)[LOADS]) {
+#pragma unroll
+  for (int i = 0; i < LOADS; ++i) {
+    *reinterpret_cast<u32x4*>(stage + soff[i]) = ra[i];
+    *reinterpret_cast<u32x4*>(stage + A_BYTES + soff[i]) = rb[i];
+  }
+}
 }  // namespace gemm
 
 template <int KIND, DType WD>
-__global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restrict__ md,
+__global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void ns_gemm_kernel(const MatDesc* __restrict__ md,
                                                          const Item* __restrict__ items,
                                                          NsParams p) {
   using namespace gemm;
@@ -174,28 +205,22 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
     P = d.Bo; Q = XTc; ld = rp;
   }
   const int64_t row0 = (int64_t)it.tm * BM, col0 = (int64_t)it.tn * BN;
-  const int nk = (int)(ld / BK);  // contraction length is the leading dimension
+  const int nk = (int)(ld / BK);  // the contraction length is the leading dimension
+  const uint16_t* Pt = P + row0 * ld;
+  const uint16_t* Qt = Q + col0 * ld;
 
-  uint4 ra[LOADS], rb[LOADS];
-  auto gload = [&](int kt) {
-    const int64_t k = (int64_t)kt * BK;
+  // Operand loads through the global address space (global_load, not flat_load,
+  // so that LDS waits do not also wait for the prefetch in flight).
+  // thread -> (tile row, 16-byte chunk) pairs of its LOADS chunks per operand
+  const int lrow = tid >> 3, lch = tid & 7;   // rows lrow + 32 i
+  gptr4 pa = (gptr4)(Pt + (int64_t)lrow * ld + lch * 8);
+  gptr4 pb = (gptr4)(Qt + (int64_t)lrow * ld + lch * 8);
+  const int64_t rstep = 32 * ld / 8;          // 32 rows, in uint4 units
+  int soff[LOADS];
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int L = i * NTHREADS + tid, r = L >> 3, ch = L & 7;
-      ra[i] = *reinterpret_cast<const uint4*>(P + (row0 + r) * ld + k + ch * 8);
-      rb[i] = *reinterpret_cast<const uint4*>(Q + (col0 + r) * ld + k + ch * 8);
-    }
-  };
-  auto sstore = [&](int stage) {
-    char* a = smem + stage * STAGE_BYTES;
-    char* b = a + BM * ROW_BYTES;
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int L = i * NTHREADS + tid, r = L >> 3, ch = L & 7;
-      *reinterpret_cast<uint4*>(a + swz(r, ch)) = ra[i];
-      *reinterpret_cast<uint4*>(b + swz(r, ch)) = rb[i];
-    }
-  };
+  for (int i = 0; i < LOADS; ++i) soff[i] = swz(lrow + 32 * i, lch);
+
+  u32x4 ra[LOADS], rb[LOADS];
 
   floatx16 acc[MI][NI];
 #pragma unroll
@@ -205,192 +230,204 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  gload(0);
-  sstore(0);
+  const int arow = wm * WM + (lane & 31), brow = wn * WN + (lane & 31);
+  const int khalf = lane >> 5;
+
+  stage_load(ra, rb, pa, pb, rstep, 0);
+  stage_store(smem, ra, rb, soff);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload(kt + 1);
+    // prefetch the next stage (the last iteration reloads its own stage into
+    // the idle buffer: harmless, and it keeps the loop free of branches)
+    stage_load(ra, rb, pa, pb, rstep, (int64_t)(kt + 1 < nk ? kt + 1 : kt) * (BK / 8));
+    // keep the prefetch at the top of the stage: the scheduler would otherwise
+    // sink it next to the LDS writes and expose the whole memory latency
+    __builtin_amdgcn_sched_barrier(0);
     const char* a = smem + (kt & 1) * STAGE_BYTES;
-    const char* b = a + BM * ROW_BYTES;
+    const char* b = a + A_BYTES;
+    // fragments of k-step ks are read while the MFMAs of k-step ks-1 run
+    bf16x8 a0[MI], b0[NI], a1[MI], b1[NI];
+    auto frag = [&](bf16x8 (&af)[MI], bf16x8 (&bf)[NI], int ks) {
+      const int ch = ks * 2 + khalf;
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int ch = ks * 2 + (lane >> 5);
-      bf16x8 af[MI], bfr[NI];
+      for (int i = 0; i < MI; ++i) af[i] = *reinterpret_cast<const bf16x8*>(a + swz(arow + i * 32, ch));
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int r = wm * WM + i * 32 + (lane & 31);
-        af[i] = *reinterpret_cast<const bf16x8*>(a + swz(r, ch));
-      }
-#pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        const int r = wn * WN + j * 32 + (lane & 31);
-        bfr[j] = *reinterpret_cast<const bf16x8*>(b + swz(r, ch));
-      }
+      for (int j = 0; j < NI; ++j) bf[j] = *reinterpret_cast<const bf16x8*>(b + swz(brow + j * 32, ch));
+    };
+    auto mma = [&](const bf16x8 (&af)[MI], const bf16x8 (&bf)[NI]) {
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore((kt + 1) & 1);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    };
+    static_assert(BK / 16 == 4, "four k-steps per stage");
+    frag(a0, b0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    frag(a1, b1, 1);
+    mma(a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    frag(a0, b0, 2);
+    mma(a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    frag(a1, b1, 3);
+    mma(a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    stage_store(smem + ((kt + 1) & 1) * STAGE_BYTES, ra, rb, soff);
     __syncthreads();
   }
-
-  // ---- stage the fp32 tile in LDS (32x32 MFMA result layout) ----
-  float* T = reinterpret_cast<float*>(smem);
-#pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int j = 0; j < NI; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        const int c = wn * WN + j * 32 + (lane & 31);
-        T[r * EPI_LD + c] = acc[i][j][v];
-      }
-  __syncthreads();
 
   const bool sym = (KIND != GEMM_APPLY);
   const bool diag = sym && it.tm == it.tn;
   const bool last = (KIND == GEMM_APPLY) && p.last;
   const float alpha = (p.iter == 0) ? *d.alpha : 1.0f;
+  const bool need_t = (sym && !diag) || (KIND == GEMM_APPLY && (!last || d.tall));
+  float* T = reinterpret_cast<float*>(smem);
 
-  // ---- pass A: row-major; final values, natural-layout outputs ----
-  constexpr int EPR = 8;                    // elements per thread per row segment
-  constexpr int TPRW = BN / EPR;            // threads per tile row (16)
-  constexpr int RPP = NTHREADS / TPRW;      // rows per pass (16)
-  constexpr int NPASS = BM / RPP;           // 8
+  // Epilogue in two halves of HM rows (the whole fp32 tile does not fit in LDS).
+  constexpr int EPR = 8;                    // consecutive elements per thread
+  constexpr int TPRW = BN / EPR;            // threads per staged row (32)
+  constexpr int RPP = NTHREADS / TPRW;      // rows per pass (8)
   const int ec = (tid % TPRW) * EPR, er = tid / TPRW;
-  float vals[NPASS][EPR];
+#pragma unroll 1
+  for (int h = 0; h < 2; ++h) {
+    if (h) __syncthreads();   // previous half fully consumed
+    if (wm == h) {
 #pragma unroll
-  for (int ps = 0; ps < NPASS; ++ps) {
-    const int r = ps * RPP + er;
-    const int64_t gi = row0 + r, gj = col0 + ec;
-    float a8[EPR];
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int q = 0; q < EPR; ++q) {
-      const int c = ec + q;
-      a8[q] = diag ? T[min(r, c) * EPI_LD + max(r, c)] : T[r * EPI_LD + c];
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int r = i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            const int c = wn * WN + j * 32 + (lane & 31);
+            T[r * EPI_LD + c] = acc[i][j][v];
+          }
     }
-    if constexpr (KIND == GEMM_GRAM) {
-      // A = alpha^2 acc (alpha folded in at the first iteration); the diagonal
-      // goes to dA in fp32, the off-diagonal part to Ao in bf16.
-      const float s2 = alpha * alpha;
+    __syncthreads();
+    const int64_t hrow0 = row0 + h * HM;
+    // ---- pass A: row-major; final values, natural-layout outputs ----
+#pragma unroll 2
+    for (int ps = 0; ps < HM / RPP; ++ps) {
+      const int r = ps * RPP + er;
+      const int64_t gi = hrow0 + r, gj = col0 + ec;
+      float v[EPR];
+      Vec<float>::load8(T + r * EPI_LD + ec, v);
+      if constexpr (KIND == GEMM_GRAM) {
+        // A = alpha^2 acc; the diagonal goes to dA (fp32), the rest to Ao (bf16)
+        const float s2 = alpha * alpha;
 #pragma unroll
-      for (int q = 0; q < EPR; ++q) {
-        const float v = a8[q] * s2;
-        const bool dg = diag && (r == ec + q);
-        if (dg) d.dA[gi] = v;
-        vals[ps][q] = dg ? 0.f : v;
-      }
-      Vec<uint16_t>::store8(d.Ao + gi * rp + gj, vals[ps]);
-    } else if constexpr (KIND == GEMM_POLY) {
-      // A^2 = dA^2 + dA Ao + Ao dA + Ao Ao;  B = b A + c A^2
-      float ao[EPR], dj[EPR];
-      Vec<uint16_t>::load8(d.Ao + gi * rp + gj, ao);
-      Vec<float>::load8(d.dA + gj, dj);
-      const float di = d.dA[gi];
+        for (int q = 0; q < EPR; ++q) {
+          v[q] *= s2;
+          if (diag && gi == gj + q) {
+            d.dA[gi] = v[q];
+            v[q] = 0.f;
+          }
+        }
+        Vec<uint16_t>::store8(d.Ao + gi * rp + gj, v);
+      } else if constexpr (KIND == GEMM_POLY) {
+        // A^2 = dA^2 + dA Ao + Ao dA + Ao Ao;  B = b A + c A^2
+        float ao[EPR], dj[EPR];
+        Vec<uint16_t>::load8(d.Ao + gi * rp + gj, ao);
+        Vec<float>::load8(d.dA + gj, dj);
+        const float di = d.dA[gi];
 #pragma unroll
-      for (int q = 0; q < EPR; ++q) {
-        const bool dg = diag && (r == ec + q);
-        if (dg) d.dB[gi] = p.b * di + p.c * (a8[q] + di * di);
-        vals[ps][q] = dg ? 0.f : p.b * ao[q] + p.c * (di * ao[q] + ao[q] * dj[q] + a8[q]);
-      }
-      Vec<uint16_t>::store8(d.Bo + gi * rp + gj, vals[ps]);
-    } else {
-      // X' = alpha ((a + dB_i) X + Bo X)
-      float x[EPR];
-      Vec<uint16_t>::load8(Xc + gi * cp + gj, x);
-      const float ai = p.a + d.dB[gi];
-#pragma unroll
-      for (int q = 0; q < EPR; ++q) vals[ps][q] = alpha * (ai * x[q] + a8[q]);
-      if (!last) {
-        Vec<uint16_t>::store8(Xo + gi * cp + gj, vals[ps]);
-      } else if (!d.tall) {
-        // oriented (gi, gj) is stored (gi, gj): W is r x c = m x n
-        const int64_t n = d.n;
-        if (gi < d.m) {
-          const float dc = d.s * p.dscale;
-          WT* W = reinterpret_cast<WT*>(d.W) + gi * n;
-          float* Dp = d.D + gi * n;
-          if ((n & 7) == 0 && gj + EPR <= n) {
-            float w[EPR], dv[EPR];
-            Vec<WT>::load8(W + gj, w);
-#pragma unroll
-            for (int q = 0; q < EPR; ++q) {
-              dv[q] = dc * vals[ps][q];
-              w[q] = w[q] * p.decay - p.lr * dv[q];
-            }
-            Vec<WT>::store8(W + gj, w);
-            if (p.write_d) Vec<float>::store8(Dp + gj, dv);
+        for (int q = 0; q < EPR; ++q) {
+          if (diag && gi == gj + q) {
+            d.dB[gi] = p.b * di + p.c * (v[q] + di * di);
+            v[q] = 0.f;
           } else {
+            v[q] = p.b * ao[q] + p.c * (di * ao[q] + ao[q] * dj[q] + v[q]);
+          }
+        }
+        Vec<uint16_t>::store8(d.Bo + gi * rp + gj, v);
+      } else {
+        // X' = alpha ((a + dB_i) X + Bo X)
+        float x[EPR];
+        Vec<uint16_t>::load8(Xc + gi * cp + gj, x);
+        const float ai = p.a + d.dB[gi];
 #pragma unroll
-            for (int q = 0; q < EPR; ++q) {
-              if (gj + q < n) {
-                const float dv = dc * vals[ps][q];
-                Vec<WT>::store1(W + gj + q, Vec<WT>::load1(W + gj + q) * p.decay - p.lr * dv);
-                if (p.write_d) Dp[gj + q] = dv;
+        for (int q = 0; q < EPR; ++q) v[q] = alpha * (ai * x[q] + v[q]);
+        if (!last) {
+          Vec<uint16_t>::store8(Xo + gi * cp + gj, v);
+        } else if (!d.tall) {
+          // oriented (gi, gj) is stored (gi, gj): W is r x c = m x n
+          const int64_t n = d.n;
+          if (gi < d.m) {
+            const float dc = d.s * p.dscale;
+            WT* W = reinterpret_cast<WT*>(d.W) + gi * n;
+            float* Dp = d.D + gi * n;
+            if ((n & 7) == 0 && gj + EPR <= n) {
+              float w[EPR], dv[EPR];
+              Vec<WT>::load8(W + gj, w);
+#pragma unroll
+              for (int q = 0; q < EPR; ++q) {
+                dv[q] = dc * v[q];
+                w[q] = w[q] * p.decay - p.lr * dv[q];
+              }
+              Vec<WT>::store8(W + gj, w);
+              if (p.write_d) Vec<float>::store8(Dp + gj, dv);
+            } else {
+#pragma unroll
+              for (int q = 0; q < EPR; ++q) {
+                if (gj + q < n) {
+                  const float dv = dc * v[q];
+                  Vec<WT>::store1(W + gj + q, Vec<WT>::load1(W + gj + q) * p.decay - p.lr * dv);
+                  if (p.write_d) Dp[gj + q] = dv;
+                }
               }
             }
           }
         }
       }
+      if (need_t) Vec<float>::store8(T + r * EPI_LD + ec, v);  // same thread, same slots
     }
-  }
-
-  // ---- pass B: transposed outputs (mirror tiles, XT, tall parameter write) ----
-  const bool need_t = (sym && !diag) || (KIND == GEMM_APPLY && (!last || d.tall));
-  if (!need_t) return;
-  __syncthreads();
+    if (!need_t) continue;
+    __syncthreads();
+    // ---- pass B: transposed outputs (mirror tiles, XT, tall parameter write) ----
+    // thread -> one tile column j, 8 consecutive staged rows per iteration
+    const int j = tid;  // BN == NTHREADS
+    const int64_t orow = col0 + j;  // transposed row
+#pragma unroll 2
+    for (int i0 = 0; i0 < HM; i0 += EPR) {
+      float v[EPR];
 #pragma unroll
-  for (int ps = 0; ps < NPASS; ++ps) {
-    const int r = ps * RPP + er;
-#pragma unroll
-    for (int q = 0; q < EPR; ++q) T[r * EPI_LD + ec + q] = vals[ps][q];
-  }
-  __syncthreads();
-  // thread -> one tile column j, 8 consecutive tile rows per pass
-  constexpr int GROUPS = NTHREADS / BN;        // 2
-  const int j = tid % BN, ig = tid / BN;
-#pragma unroll
-  for (int ps = 0; ps < BM / (EPR * GROUPS); ++ps) {
-    const int i0 = (ps * GROUPS + ig) * EPR;
-    float v[EPR];
-#pragma unroll
-    for (int q = 0; q < EPR; ++q) v[q] = T[(i0 + q) * EPI_LD + j];
-    const int64_t orow = col0 + j;       // transposed row
-    const int64_t ocol = row0 + i0;      // transposed column start
-    if constexpr (KIND == GEMM_GRAM) {
-      Vec<uint16_t>::store8(d.Ao + orow * rp + ocol, v);
-    } else if constexpr (KIND == GEMM_POLY) {
-      Vec<uint16_t>::store8(d.Bo + orow * rp + ocol, v);
-    } else {
-      if (!last) {
-        Vec<uint16_t>::store8(XTo + orow * rp + ocol, v);
+      for (int q = 0; q < EPR; ++q) v[q] = T[(i0 + q) * EPI_LD + j];
+      const int64_t ocol = hrow0 + i0;  // transposed column start
+      if constexpr (KIND == GEMM_GRAM) {
+        Vec<uint16_t>::store8(d.Ao + orow * rp + ocol, v);
+      } else if constexpr (KIND == GEMM_POLY) {
+        Vec<uint16_t>::store8(d.Bo + orow * rp + ocol, v);
       } else {
-        // tall: oriented (i, j) is stored (j, i); W is c x r = m x n
-        const int64_t n = d.n;
-        if (orow < d.m) {
-          const float dc = d.s * p.dscale;
-          WT* W = reinterpret_cast<WT*>(d.W) + orow * n;
-          float* Dp = d.D + orow * n;
-          if ((n & 7) == 0 && ocol + EPR <= n) {
-            float w[EPR], dv[EPR];
-            Vec<WT>::load8(W + ocol, w);
+        if (!last) {
+          Vec<uint16_t>::store8(XTo + orow * rp + ocol, v);
+        } else {
+          // tall: oriented (i, j) is stored (j, i); W is c x r = m x n
+          const int64_t n = d.n;
+          if (orow < d.m) {
+            const float dc = d.s * p.dscale;
+            WT* W = reinterpret_cast<WT*>(d.W) + orow * n;
+            float* Dp = d.D + orow * n;
+            if ((n & 7) == 0 && ocol + EPR <= n) {
+              float w[EPR], dv[EPR];
+              Vec<WT>::load8(W + ocol, w);
 #pragma unroll
-            for (int q = 0; q < EPR; ++q) {
-              dv[q] = dc * v[q];
-              w[q] = w[q] * p.decay - p.lr * dv[q];
-            }
-            Vec<WT>::store8(W + ocol, w);
-            if (p.write_d) Vec<float>::store8(Dp + ocol, dv);
-          } else {
+              for (int q = 0; q < EPR; ++q) {
+                dv[q] = dc * v[q];
+                w[q] = w[q] * p.decay - p.lr * dv[q];
+              }
+              Vec<WT>::store8(W + ocol, w);
+              if (p.write_d) Vec<float>::store8(Dp + ocol, dv);
+            } else {
 #pragma unroll
-            for (int q = 0; q < EPR; ++q) {
-              if (ocol + q < n) {
-                const float dv = dc * v[q];
-                Vec<WT>::store1(W + ocol + q, Vec<WT>::load1(W + ocol + q) * p.decay - p.lr * dv);
-                if (p.write_d) Dp[ocol + q] = dv;
+              for (int q = 0; q < EPR; ++q) {
+                if (ocol + q < n) {
+                  const float dv = dc * v[q];
+                  Vec<WT>::store1(W + ocol + q, Vec<WT>::load1(W + ocol + q) * p.decay - p.lr * dv);
+                  if (p.write_d) Dp[ocol + q] = dv;
+                }
               }
             }
           }

@@ -105,7 +105,7 @@ hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item
                           int32_t nitems, const NsParams& p, hipStream_t s);
 
 // GEMM tile edge used by the NS5 kernels; rp and cp are multiples of it.
-constexpr int kNsTile = 128;
+constexpr int kNsTile = 256;
 // Prologue tile edge.
 constexpr int kPrologueTile = 64;
 // Row block of the tall statistics pass.

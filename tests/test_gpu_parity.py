@@ -88,7 +88,8 @@ def test_variants(flag, t):
 
 def test_several_workspace_chunks():
     shapes = [(256, 512), (512, 256), (128, 640), (200, 200), (256, 512)]
-    one = 8 * 256 * 640 + 6 * 256 * 256 + 4096
+    # a budget that holds the largest single matrix but not all of them
+    one = max(prm.workspace_bytes([s], prm.config_default()) for s in shapes)
     cfg = prm.config_default(K=2, lr=0.01, wd=0.01, workspace_budget_bytes=one)
     assert prm.workspace_bytes(shapes, cfg) < prm.workspace_bytes(shapes, prm.config_default())
     rho, res = run_one_step(shapes, cfg, 0, workload_id=92)
