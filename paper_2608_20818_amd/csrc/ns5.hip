@@ -14,8 +14,8 @@
 //    (alpha^2) and the first apply (alpha) epilogues.
 //  * ns_alpha: fixed-order reduction of the tile sums into alpha.
 //  * ns_gemm: C = P Q^T on bf16 operands with fp32 MFMA accumulation
-//    (v_mfma_f32_32x32x16_bf16), 256 x 256 tiles, BK = 64, LDS double buffer
-//    with an XOR swizzle.  Every product of the iteration has this NT form:
+//    (v_mfma_f32_32x32x16_bf16), 256 x 256 tiles, BK = 64, operands streamed
+//    into a double LDS buffer by direct global-to-LDS loads.  Every product of the iteration has this NT form:
 //      Gram   A   = X X^T              (upper tiles only, mirrored)
 //      square A^2 = A A^T              (A is symmetric; upper tiles, mirrored)
 //      apply  B X = B (XT)^T           (XT is the transposed copy of X)
@@ -27,6 +27,8 @@
 //    the parameter write W <- (1 - eta lambda) W - eta s O^{-1}(X_5).
 // The workspace is padded to whole tiles and the padding stays exactly zero
 // through every iteration, so the GEMMs need no bounds checks.
+#include <type_traits>
+
 #include "prm_device.h"
 
 namespace prm {
@@ -130,9 +132,13 @@ __global__ __launch_bounds__(256) void ns_alpha_kernel(const MatDesc* __restrict
 //
 // Work-group tile 256 x 256, four waves in a 2 x 2 grid, each wave owning a
 // 128 x 128 block as 4 x 4 MFMA 32x32x16 accumulators (256 fp32 per lane).
-// K advances in stages of 64: global loads of stage k+1 are issued into
-// registers before stage k is computed from LDS, then written to the other
-// LDS buffer.  Per stage and wave: 64 MFMAs against 32 fragment reads.
+// K advances in stages of 64 through two LDS buffers.  Operands move from
+// global memory straight into LDS (global_load_lds_dwordx4): each wave
+// instruction fills 1 KB (8 tile rows) in lane order, and the XOR swizzle of
+// the 16-byte chunks is obtained by choosing which global chunk each lane
+// fetches.  Stage k+1 streams into one buffer while stage k is read from the
+// other; the two buffers are distinct LDS arrays, so fragment reads never wait
+// for the stage in flight.
 // ---------------------------------------------------------------------------
 namespace gemm {
 constexpr int BM = kNsTile, BN = kNsTile, BK = 64;
@@ -142,51 +148,32 @@ constexpr int MI = WM / 32, NI = WN / 32;
 constexpr int ROW_BYTES = BK * 2;                       // 128 B per tile row
 constexpr int A_BYTES = BM * ROW_BYTES;                 // 32 KB
 constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;      // 64 KB
-constexpr int OP_BYTES = 2 * STAGE_BYTES;               // 128 KB
-constexpr int HM = BM / 2;                              // epilogue works on half tiles
-constexpr int EPI_LD = BN + 8;                          // fp32 words per staged row
-constexpr int EPI_BYTES = HM * EPI_LD * 4;              // 132 KB
-constexpr int LDS_BYTES = OP_BYTES > EPI_BYTES ? OP_BYTES : EPI_BYTES;
-constexpr int LOADS = BM * (BK / 8) / NTHREADS;         // 16-byte chunks per thread per operand
+constexpr int DMA_PER_WAVE = BM / 8 / 4;                // 1 KB wave loads per operand per stage
+constexpr int QM = 64;                                  // epilogue quarter rows
+constexpr int EPI_LD = BN;                              // fp32 words per staged row
+static_assert(QM * EPI_LD * 4 <= STAGE_BYTES, "quarter tile fits a stage buffer");
 
-// byte offset of 16-byte chunk `ch` of tile row `r` (XOR swizzle over 8 chunks)
+// byte offset of 16-byte chunk `ch` of tile row `r`: XOR swizzle of the eight
+// 16-byte chunks of a row, so that fragment reads (one row per lane, same chunk)
+// spread over the banks.
 __device__ __forceinline__ int swz(int r, int ch) { return r * ROW_BYTES + ((ch ^ (r & 7)) << 4); }
 
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef const __attribute__((address_space(1))) u32x4* gptr4;
-
-// One stage of both operands into registers: chunk i of this thread is tile
-// row (thread/8 + 32 i), 16-byte chunk thread%8, at uint4 offset `ko` along K.
-__device__ __forceinline__ void stage_load(u32x4 (&ra)[LOADS], u32x4 (&rb)[LOADS], gptr4 pa,
-                                           gptr4 pb, int64_t rstep, int64_t ko) {
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) {
-    ra[i] = pa[i * rstep + ko];
-    rb[i] = pb[i * rstep + ko];
-  }
-}
-
-__device__ __forceinline__ void stage_store(char* stage, const u32x4 (&ra)[LOADS],
-                                            const u32x4 (&rb)[LOADS], const int (&soff)[LOADS]) {
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) {
-    *reinterpret_cast<u32x4*>(stage + soff[i]) = ra[i];
-    *reinterpret_cast<u32x4*>(stage + A_BYTES + soff[i]) = rb[i];
-  }
-}
+typedef __attribute__((address_space(3))) void* lds_ptr;
 }  // namespace gemm
 
 template <int KIND, DType WD>
-__global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void ns_gemm_kernel(const MatDesc* __restrict__ md,
+__global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restrict__ md,
                                                          const Item* __restrict__ items,
                                                          NsParams p) {
   using namespace gemm;
   using WT = typename NsStore<WD>::T;
-  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
+  __shared__ __attribute__((aligned(16))) char s0[STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) char s1[STAGE_BYTES];
 
   const Item it = items[blockIdx.x];
   const MatDesc& d = md[it.mat];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const bool even = (p.iter & 1) == 0;
   const uint16_t* Xc = even ? d.X : d.Xn;
@@ -205,22 +192,22 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
     P = d.Bo; Q = XTc; ld = rp;
   }
   const int64_t row0 = (int64_t)it.tm * BM, col0 = (int64_t)it.tn * BN;
-  const int nk = (int)(ld / BK);  // the contraction length is the leading dimension
-  const uint16_t* Pt = P + row0 * ld;
-  const uint16_t* Qt = Q + col0 * ld;
+  const int nk = (int)(ld / BK);  // even: the padded contraction length is a multiple of the tile
 
-  // Operand loads through the global address space (global_load, not flat_load,
-  // so that LDS waits do not also wait for the prefetch in flight).
-  // thread -> (tile row, 16-byte chunk) pairs of its LOADS chunks per operand
-  const int lrow = tid >> 3, lch = tid & 7;   // rows lrow + 32 i
-  gptr4 pa = (gptr4)(Pt + (int64_t)lrow * ld + lch * 8);
-  gptr4 pb = (gptr4)(Qt + (int64_t)lrow * ld + lch * 8);
-  const int64_t rstep = 32 * ld / 8;          // 32 rows, in uint4 units
-  int soff[LOADS];
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) soff[i] = swz(lrow + 32 * i, lch);
-
-  u32x4 ra[LOADS], rb[LOADS];
+  // DMA sources: wave instruction q covers tile rows 64 wave + 8 q + lane / 8;
+  // lane fills physical chunk lane % 8, i.e. logical chunk (lane % 8) ^ (row % 8).
+  const int64_t lane_off = (int64_t)(lane >> 3) * ld + (((lane & 7) ^ (lane >> 3)) << 3);
+  const uint16_t* srcA = P + (row0 + 64 * wave) * ld + lane_off;
+  const uint16_t* srcB = Q + (col0 + 64 * wave) * ld + lane_off;
+  // One 1 KB wave load of the stage: block q < 8 of operand A, q >= 8 of B.
+  auto dma1 = [&](char* stage, int64_t k, int q) {
+    const bool isb = q >= DMA_PER_WAVE;
+    const int qq = isb ? q - DMA_PER_WAVE : q;
+    __builtin_amdgcn_global_load_lds((const void*)((isb ? srcB : srcA) + (int64_t)(8 * qq) * ld + k),
+                                     (lds_ptr)(stage + (isb ? A_BYTES : 0) + (DMA_PER_WAVE * wave + qq) * 1024),
+                                     16, 0, 0);
+  };
+  constexpr int NDMA = 2 * DMA_PER_WAVE;  // 16 wave loads per stage
 
   floatx16 acc[MI][NI];
 #pragma unroll
@@ -233,49 +220,56 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
   const int arow = wm * WM + (lane & 31), brow = wn * WN + (lane & 31);
   const int khalf = lane >> 5;
 
-  stage_load(ra, rb, pa, pb, rstep, 0);
-  stage_store(smem, ra, rb, soff);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    // prefetch the next stage (the last iteration reloads its own stage into
-    // the idle buffer: harmless, and it keeps the loop free of branches)
-    stage_load(ra, rb, pa, pb, rstep, (int64_t)(kt + 1 < nk ? kt + 1 : kt) * (BK / 8));
-    // keep the prefetch at the top of the stage: the scheduler would otherwise
-    // sink it next to the LDS writes and expose the whole memory latency
-    __builtin_amdgcn_sched_barrier(0);
-    const char* a = smem + (kt & 1) * STAGE_BYTES;
-    const char* b = a + A_BYTES;
-    // fragments of k-step ks are read while the MFMAs of k-step ks-1 run
-    bf16x8 a0[MI], b0[NI], a1[MI], b1[NI];
-    auto frag = [&](bf16x8 (&af)[MI], bf16x8 (&bf)[NI], int ks) {
+  // Compute one stage from `cur` while streaming stage `knext` (if >= 0) into
+  // `nxt`.  The vector-memory path accepts about one 1 KB wave load per 16
+  // cycles, so the 16 loads are spread between MFMA sub-groups (4 at the start,
+  // then one per 4 MFMAs over the first three k-steps) instead of stalling the
+  // in-order issue behind a burst.  Each sub-group also reads 2 of the 8
+  // fragments of the next k-step.
+  auto stage_compute = [&](const char* cur, char* nxt, int knext) {
+    const char* a = cur;
+    const char* b = cur + A_BYTES;
+    const int64_t kn = (int64_t)knext * BK;
+    const bool more = knext >= 0;
+    bf16x8 fa[2][MI], fb[2][NI];
+    auto rd = [&](int set, int i, int ks) {
       const int ch = ks * 2 + khalf;
-#pragma unroll
-      for (int i = 0; i < MI; ++i) af[i] = *reinterpret_cast<const bf16x8*>(a + swz(arow + i * 32, ch));
-#pragma unroll
-      for (int j = 0; j < NI; ++j) bf[j] = *reinterpret_cast<const bf16x8*>(b + swz(brow + j * 32, ch));
+      fa[set][i] = *reinterpret_cast<const bf16x8*>(a + swz(arow + i * 32, ch));
+      fb[set][i] = *reinterpret_cast<const bf16x8*>(b + swz(brow + i * 32, ch));
     };
-    auto mma = [&](const bf16x8 (&af)[MI], const bf16x8 (&bf)[NI]) {
+    if (more) {
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
+      for (int q = 0; q < 4; ++q) dma1(nxt, kn, q);
+    }
+#pragma unroll
+    for (int i = 0; i < MI; ++i) rd(0, i, 0);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int cs = ks & 1;
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {          // sub-group: row block i, 4 MFMAs
+        if (ks < 3) {
+          if (more) dma1(nxt, kn, 4 + ks * 4 + i);
+          rd(cs ^ 1, i, ks + 1);
+        }
 #pragma unroll
         for (int j = 0; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
-    };
-    static_assert(BK / 16 == 4, "four k-steps per stage");
-    frag(a0, b0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    frag(a1, b1, 1);
-    mma(a0, b0);
-    __builtin_amdgcn_sched_barrier(0);
-    frag(a0, b0, 2);
-    mma(a1, b1);
-    __builtin_amdgcn_sched_barrier(0);
-    frag(a1, b1, 3);
-    mma(a0, b0);
-    __builtin_amdgcn_sched_barrier(0);
-    mma(a1, b1);
-    __builtin_amdgcn_sched_barrier(0);
-    stage_store(smem + ((kt + 1) & 1) * STAGE_BYTES, ra, rb, soff);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cs][i], fb[cs][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+  static_assert(NDMA == 16 && BK / 16 == 4 && MI == 4, "schedule assumes 16 loads, 4 k-steps, 4 row blocks");
+
+  // stage 0 up front, then ping-pong: s0 holds even stages, s1 odd ones
+#pragma unroll
+  for (int q = 0; q < NDMA; ++q) dma1(s0, 0, q);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    stage_compute(s0, s1, kt + 1);
+    __syncthreads();  // stage kt+1 has landed; every wave is done with s0
+    stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1);
     __syncthreads();
   }
 
@@ -284,35 +278,49 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
   const bool last = (KIND == GEMM_APPLY) && p.last;
   const float alpha = (p.iter == 0) ? *d.alpha : 1.0f;
   const bool need_t = (sym && !diag) || (KIND == GEMM_APPLY && (!last || d.tall));
-  float* T = reinterpret_cast<float*>(smem);
 
-  // Epilogue in two halves of HM rows (the whole fp32 tile does not fit in LDS).
+  // Epilogue in four quarters of QM rows, staged alternately in s0 and s1.
   constexpr int EPR = 8;                    // consecutive elements per thread
   constexpr int TPRW = BN / EPR;            // threads per staged row (32)
   constexpr int RPP = NTHREADS / TPRW;      // rows per pass (8)
+  constexpr int NPASS = QM / RPP;           // 8
   const int ec = (tid % TPRW) * EPR, er = tid / TPRW;
-#pragma unroll 1
-  for (int h = 0; h < 2; ++h) {
-    if (h) __syncthreads();   // previous half fully consumed
-    if (wm == h) {
+  // the quarter index is a compile-time constant: acc[] must be indexed statically
+  auto quarter = [&](auto hc) {
+    constexpr int h = decltype(hc)::value;
+    float* T = reinterpret_cast<float*>((h & 1) ? s1 : s0);
+    if (h >= 2) __syncthreads();  // quarter h-2 is fully consumed
+    if (wm == (h >> 1)) {
+      const int ib = (h & 1) * 2;  // the two 32-row MFMA blocks of this quarter
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < NI; ++j)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int r = i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
             const int c = wn * WN + j * 32 + (lane & 31);
-            T[r * EPI_LD + c] = acc[i][j][v];
+            T[r * EPI_LD + c] = acc[ib + i][j][v];
           }
     }
+    const int64_t qrow0 = row0 + h * QM;
+    // inputs of the natural-layout pass, issued before the barrier
+    float xin[NPASS][EPR];
+    if constexpr (KIND == GEMM_APPLY) {
+#pragma unroll
+      for (int ps = 0; ps < NPASS; ++ps)
+        Vec<uint16_t>::load8(Xc + (qrow0 + ps * RPP + er) * cp + col0 + ec, xin[ps]);
+    } else if constexpr (KIND == GEMM_POLY) {
+#pragma unroll
+      for (int ps = 0; ps < NPASS; ++ps)
+        Vec<uint16_t>::load8(d.Ao + (qrow0 + ps * RPP + er) * rp + col0 + ec, xin[ps]);
+    }
     __syncthreads();
-    const int64_t hrow0 = row0 + h * HM;
     // ---- pass A: row-major; final values, natural-layout outputs ----
-#pragma unroll 2
-    for (int ps = 0; ps < HM / RPP; ++ps) {
+#pragma unroll
+    for (int ps = 0; ps < NPASS; ++ps) {
       const int r = ps * RPP + er;
-      const int64_t gi = hrow0 + r, gj = col0 + ec;
+      const int64_t gi = qrow0 + r, gj = col0 + ec;
       float v[EPR];
       Vec<float>::load8(T + r * EPI_LD + ec, v);
       if constexpr (KIND == GEMM_GRAM) {
@@ -329,27 +337,25 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
         Vec<uint16_t>::store8(d.Ao + gi * rp + gj, v);
       } else if constexpr (KIND == GEMM_POLY) {
         // A^2 = dA^2 + dA Ao + Ao dA + Ao Ao;  B = b A + c A^2
-        float ao[EPR], dj[EPR];
-        Vec<uint16_t>::load8(d.Ao + gi * rp + gj, ao);
+        float dj[EPR];
         Vec<float>::load8(d.dA + gj, dj);
         const float di = d.dA[gi];
 #pragma unroll
         for (int q = 0; q < EPR; ++q) {
+          const float ao = xin[ps][q];
           if (diag && gi == gj + q) {
             d.dB[gi] = p.b * di + p.c * (v[q] + di * di);
             v[q] = 0.f;
           } else {
-            v[q] = p.b * ao[q] + p.c * (di * ao[q] + ao[q] * dj[q] + v[q]);
+            v[q] = p.b * ao + p.c * (di * ao + ao * dj[q] + v[q]);
           }
         }
         Vec<uint16_t>::store8(d.Bo + gi * rp + gj, v);
       } else {
         // X' = alpha ((a + dB_i) X + Bo X)
-        float x[EPR];
-        Vec<uint16_t>::load8(Xc + gi * cp + gj, x);
         const float ai = p.a + d.dB[gi];
 #pragma unroll
-        for (int q = 0; q < EPR; ++q) v[q] = alpha * (ai * x[q] + v[q]);
+        for (int q = 0; q < EPR; ++q) v[q] = alpha * (ai * xin[ps][q] + v[q]);
         if (!last) {
           Vec<uint16_t>::store8(Xo + gi * cp + gj, v);
         } else if (!d.tall) {
@@ -384,18 +390,18 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
       }
       if (need_t) Vec<float>::store8(T + r * EPI_LD + ec, v);  // same thread, same slots
     }
-    if (!need_t) continue;
+    if (!need_t) return;
     __syncthreads();
     // ---- pass B: transposed outputs (mirror tiles, XT, tall parameter write) ----
     // thread -> one tile column j, 8 consecutive staged rows per iteration
     const int j = tid;  // BN == NTHREADS
     const int64_t orow = col0 + j;  // transposed row
-#pragma unroll 2
-    for (int i0 = 0; i0 < HM; i0 += EPR) {
+#pragma unroll
+    for (int i0 = 0; i0 < QM; i0 += EPR) {
       float v[EPR];
 #pragma unroll
       for (int q = 0; q < EPR; ++q) v[q] = T[(i0 + q) * EPI_LD + j];
-      const int64_t ocol = hrow0 + i0;  // transposed column start
+      const int64_t ocol = qrow0 + i0;  // transposed column start
       if constexpr (KIND == GEMM_GRAM) {
         Vec<uint16_t>::store8(d.Ao + orow * rp + ocol, v);
       } else if constexpr (KIND == GEMM_POLY) {
@@ -434,7 +440,12 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
         }
       }
     }
-  }
+  };
+  static_assert(BM / QM == 4, "four quarters");
+  quarter(std::integral_constant<int, 0>{});
+  quarter(std::integral_constant<int, 1>{});
+  quarter(std::integral_constant<int, 2>{});
+  quarter(std::integral_constant<int, 3>{});
 }
 
 // ---------------------------------------------------------------------------

@@ -212,6 +212,41 @@ int make_plan(int32_t n_mats, const int64_t* rows, const int64_t* cols, const pr
   return PRM_OK;
 }
 
+// Work groups are dispatched round-robin over the eight XCDs (group b runs on
+// XCD b mod 8), and each XCD has its own L2.  A GEMM work list therefore keeps
+// all tiles of one matrix on one XCD (matrix k of the chunk -> XCD k mod 8) and
+// orders them in super-rows of kSuperRows tile rows, so that the ~32 groups an
+// XCD runs at once share a few row and column panels of the operands.  The
+// per-XCD lists are then interleaved into one launch order.
+constexpr int kXcds = 8;
+constexpr int kSuperRows = 4;
+
+// Tiles (tm, tn) of a tr x tc grid (upper triangle only if `upper`) in
+// super-row order.
+void tile_order(int32_t mat, int32_t tr, int32_t tc, bool upper, std::vector<Item>& out) {
+  for (int32_t a0 = 0; a0 < tr; a0 += kSuperRows) {
+    const int32_t a1 = std::min(tr, a0 + kSuperRows);
+    for (int32_t b = upper ? a0 : 0; b < tc; ++b)
+      for (int32_t a = a0; a < a1; ++a)
+        if (!upper || b >= a) out.push_back(Item{mat, a, b, 0});
+  }
+}
+
+// Interleave per-XCD item lists so that list x lands on positions = x mod 8
+// while every list still has items.
+std::vector<Item> interleave_xcd(const std::vector<std::vector<Item>>& per) {
+  std::vector<Item> out;
+  size_t total = 0;
+  for (const auto& v : per) total += v.size();
+  out.reserve(total);
+  std::vector<size_t> pos(per.size(), 0);
+  while (out.size() < total) {
+    for (size_t x = 0; x < per.size(); ++x)
+      if (pos[x] < per[x].size()) out.push_back(per[x][pos[x]++]);
+  }
+  return out;
+}
+
 // Work lists (host side); built only by prm_init.
 void build_lists(Plan& P, const prm_config* cfg) {
   // row-wise wide classes
@@ -256,20 +291,22 @@ void build_lists(Plan& P, const prm_config* cfg) {
       const int64_t pn = (P.tall[i] ? P.rp[i] : P.cp[i]) / kPrologueTile;
       for (int32_t a = 0; a < pm; ++a)
         for (int32_t b = 0; b < pn; ++b) ch.prologue.push_back(Item{i, a, b, 0});
-      const int32_t tr = (int32_t)(P.rp[i] / kNsTile), tc = (int32_t)(P.cp[i] / kNsTile);
-      for (int32_t a = 0; a < tr; ++a)
-        for (int32_t b = a; b < tr; ++b) {
-          ch.gram.push_back(Item{i, a, b, 0});
-          ch.poly.push_back(Item{i, a, b, 0});
-        }
-      for (int32_t a = 0; a < tr; ++a)
-        for (int32_t b = 0; b < tc; ++b) ch.apply.push_back(Item{i, a, b, 0});
       const double r = (double)std::min(P.m[i], P.nn[i]), c = (double)std::max(P.m[i], P.nn[i]);
       ch.elems += r * c;
       ch.flops_gram += 2 * r * r * c;
       ch.flops_poly += 2 * r * r * r;
       ch.flops_apply += 2 * r * r * c;
     }
+    std::vector<std::vector<Item>> g(kXcds), a(kXcds);
+    for (size_t k = 0; k < ch.mats.size(); ++k) {
+      const int i = ch.mats[k];
+      const int32_t tr = (int32_t)(P.rp[i] / kNsTile), tc = (int32_t)(P.cp[i] / kNsTile);
+      tile_order(i, tr, tr, true, g[k % kXcds]);
+      tile_order(i, tr, tc, false, a[k % kXcds]);
+    }
+    ch.gram = interleave_xcd(g);
+    ch.poly = ch.gram;
+    ch.apply = interleave_xcd(a);
   }
   (void)cfg;
   // flatten
