@@ -159,6 +159,14 @@ static_assert(QM * EPI_LD * 4 <= STAGE_BYTES, "quarter tile fits a stage buffer"
 __device__ __forceinline__ int swz(int r, int ch) { return r * ROW_BYTES + ((ch ^ (r & 7)) << 4); }
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(1))) u32x4* gptr4;
+
+// fp32 staging tile of the epilogue (QM x 256, no padding): column c of row r
+// is stored at c ^ (8 * ((r / 8) % 8)), which keeps aligned 8-column groups
+// contiguous (row-major pass) and makes the column pass, where 8 lanes read 8
+// row groups of one column, free of bank conflicts.
+__device__ __forceinline__ int tix(int r, int c) { return r * EPI_LD + (c ^ (((r >> 3) & 7) << 3)); }
 }  // namespace gemm
 
 template <int KIND, DType WD>
@@ -285,44 +293,52 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   constexpr int RPP = NTHREADS / TPRW;      // rows per pass (8)
   constexpr int NPASS = QM / RPP;           // 8
   const int ec = (tid % TPRW) * EPR, er = tid / TPRW;
-  // the quarter index is a compile-time constant: acc[] must be indexed statically
-  auto quarter = [&](auto hc) {
-    constexpr int h = decltype(hc)::value;
+  // Accumulator rows of MFMA blocks IB, IB+1 (one quarter) into the staging tile.
+  // acc[] needs static indices, so the block offset is a template parameter.
+  auto stage_acc = [&](float* T, auto ibc) {
+    constexpr int IB = decltype(ibc)::value;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          const int c = wn * WN + j * 32 + (lane & 31);
+          T[tix(r, c)] = acc[IB + i][j][v];
+        }
+  };
+  constexpr int NQ = BM / QM;
+#pragma unroll 1
+  for (int h = 0; h < NQ; ++h) {
     float* T = reinterpret_cast<float*>((h & 1) ? s1 : s0);
     if (h >= 2) __syncthreads();  // quarter h-2 is fully consumed
     if (wm == (h >> 1)) {
-      const int ib = (h & 1) * 2;  // the two 32-row MFMA blocks of this quarter
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int r = i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-            const int c = wn * WN + j * 32 + (lane & 31);
-            T[r * EPI_LD + c] = acc[ib + i][j][v];
-          }
+      if (h & 1) stage_acc(T, std::integral_constant<int, 2>{});
+      else stage_acc(T, std::integral_constant<int, 0>{});
     }
     const int64_t qrow0 = row0 + h * QM;
-    // inputs of the natural-layout pass, issued before the barrier
-    float xin[NPASS][EPR];
-    if constexpr (KIND == GEMM_APPLY) {
+    // inputs of the natural-layout pass (X for apply, Ao for the square)
+    u32x4 xin[NPASS];  // packed bf16
+    if constexpr (KIND != GEMM_GRAM) {
+      const uint16_t* src = (KIND == GEMM_APPLY) ? Xc : d.Ao;
+      const int64_t lds_ = (KIND == GEMM_APPLY) ? cp : rp;
 #pragma unroll
       for (int ps = 0; ps < NPASS; ++ps)
-        Vec<uint16_t>::load8(Xc + (qrow0 + ps * RPP + er) * cp + col0 + ec, xin[ps]);
-    } else if constexpr (KIND == GEMM_POLY) {
-#pragma unroll
-      for (int ps = 0; ps < NPASS; ++ps)
-        Vec<uint16_t>::load8(d.Ao + (qrow0 + ps * RPP + er) * rp + col0 + ec, xin[ps]);
+        xin[ps] = *(gptr4)(src + (qrow0 + ps * RPP + er) * lds_ + col0 + ec);
     }
+    auto xval = [&](int ps, int q) {
+      const uint32_t w = xin[ps][q >> 1];
+      return bf2f((q & 1) ? (w >> 16) : (w & 0xffffu));
+    };
     __syncthreads();
     // ---- pass A: row-major; final values, natural-layout outputs ----
-#pragma unroll
+#pragma unroll 2
     for (int ps = 0; ps < NPASS; ++ps) {
       const int r = ps * RPP + er;
       const int64_t gi = qrow0 + r, gj = col0 + ec;
       float v[EPR];
-      Vec<float>::load8(T + r * EPI_LD + ec, v);
+      Vec<float>::load8(T + tix(r, ec), v);
       if constexpr (KIND == GEMM_GRAM) {
         // A = alpha^2 acc; the diagonal goes to dA (fp32), the rest to Ao (bf16)
         const float s2 = alpha * alpha;
@@ -342,7 +358,7 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
         const float di = d.dA[gi];
 #pragma unroll
         for (int q = 0; q < EPR; ++q) {
-          const float ao = xin[ps][q];
+          const float ao = xval(ps, q);
           if (diag && gi == gj + q) {
             d.dB[gi] = p.b * di + p.c * (v[q] + di * di);
             v[q] = 0.f;
@@ -355,7 +371,7 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
         // X' = alpha ((a + dB_i) X + Bo X)
         const float ai = p.a + d.dB[gi];
 #pragma unroll
-        for (int q = 0; q < EPR; ++q) v[q] = alpha * (ai * xin[ps][q] + v[q]);
+        for (int q = 0; q < EPR; ++q) v[q] = alpha * (ai * xval(ps, q) + v[q]);
         if (!last) {
           Vec<uint16_t>::store8(Xo + gi * cp + gj, v);
         } else if (!d.tall) {
@@ -388,19 +404,23 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
           }
         }
       }
-      if (need_t) Vec<float>::store8(T + r * EPI_LD + ec, v);  // same thread, same slots
+      if (need_t) Vec<float>::store8(T + tix(r, ec), v);  // same thread, same slots
     }
-    if (!need_t) return;
+    if (!need_t) continue;
     __syncthreads();
     // ---- pass B: transposed outputs (mirror tiles, XT, tall parameter write) ----
-    // thread -> one tile column j, 8 consecutive staged rows per iteration
-    const int j = tid;  // BN == NTHREADS
-    const int64_t orow = col0 + j;  // transposed row
-#pragma unroll
-    for (int i0 = 0; i0 < QM; i0 += EPR) {
+    // 8 lanes cover one transposed row segment of QM elements (one 128-byte
+    // line for bf16): thread -> tile column j = 32 pass + tid / 8, staged rows
+    // i0 .. i0+7 with i0 = 8 (tid % 8)
+    static_assert(QM == 8 * EPR, "8 lanes per transposed row segment");
+    const int i0 = (tid & 7) * EPR;
+#pragma unroll 2
+    for (int jp = 0; jp < BN; jp += NTHREADS / 8) {
+      const int j = jp + (tid >> 3);
+      const int64_t orow = col0 + j;  // transposed row
       float v[EPR];
 #pragma unroll
-      for (int q = 0; q < EPR; ++q) v[q] = T[(i0 + q) * EPI_LD + j];
+      for (int q = 0; q < EPR; ++q) v[q] = T[tix(i0 + q, j)];
       const int64_t ocol = qrow0 + i0;  // transposed column start
       if constexpr (KIND == GEMM_GRAM) {
         Vec<uint16_t>::store8(d.Ao + orow * rp + ocol, v);
@@ -440,12 +460,7 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
         }
       }
     }
-  };
-  static_assert(BM / QM == 4, "four quarters");
-  quarter(std::integral_constant<int, 0>{});
-  quarter(std::integral_constant<int, 1>{});
-  quarter(std::integral_constant<int, 2>{});
-  quarter(std::integral_constant<int, 3>{});
+  }
 }
 
 // ---------------------------------------------------------------------------
