@@ -1,0 +1,125 @@
+"""Full-size parity on the DiT-4B-shaped weight set (160 matrices, 5.44 G
+elements, bf16 W and G, fp32 M) in the launch configuration bench.py times.
+
+The oracle cannot run the whole set, so it checks sampled outputs it can
+compute one by one:
+* refresh step (t = 0): 48 oriented rows of NS5 for the five matrices of
+  block 0, from the eigendecomposition closed form of the oracle (pinned to the
+  five-iteration map on small inputs), relative Frobenius error <= 2e-2 over
+  the sampled rows;
+* row-wise step (t = 1): 64 oriented rows (stored columns for the tall MLP
+  down projection) of every sampled matrix, error <= 1e-5;
+* momentum rows <= 1e-6; bf16 W rows within half an ulp plus eta |D - D_oracle|.
+The non-debug prm_step (what bench.py times) must produce bitwise the same W
+and M as prm_step_debug on the same inputs.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import paper_2608_20818_amd as prm  # noqa: E402
+import prm_case as pc  # noqa: E402
+import synth  # noqa: E402
+from oracle import prm_oracle as po  # noqa: E402
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+WL_IDX = 2
+WL = synth.WORKLOADS[WL_IDX]
+
+
+def make_set(step):
+    W, M, G = [], [], []
+    for i, (m, n) in enumerate(WL.shapes):
+        d = synth.device_matrix(WL_IDX, i, m, n, synth.rank_of(WL, m, n), param_dtype=WL.param_dtype,
+                                grad_dtype=WL.grad_dtype, device="cuda", beta=WL.beta, step=step)
+        W.append(d["W"])
+        M.append(d["M"])
+        G.append(d["G"])
+    torch.cuda.synchronize()
+    return W, M, G
+
+
+def config():
+    return prm.config_default(K=WL.K, lr=WL.lr, wd=WL.wd, gamma=WL.gamma, beta=WL.beta,
+                              param_dtype=prm.BF16, grad_dtype=prm.BF16)
+
+
+def run(step, sample):
+    """One step at the given t over the whole set; returns host copies of the
+    sampled matrices' inputs and outputs, and checks debug vs timed bitwise."""
+    cfg = config()
+    shapes = list(WL.shapes)
+    W, M, G = make_set(step)
+    host_in = {i: (pc.to_host(W[i]), pc.to_host(M[i]), pc.to_host(G[i])) for i in sample}
+    W2 = [w.clone() for w in W]
+    M2 = [m.clone() for m in M]
+    D = [torch.empty(s, dtype=torch.float32, device="cuda") for s in shapes]
+    with prm.Optimizer(shapes, cfg) as opt:
+        rho = opt.step(W, G, M, step, directions=D)
+        rho2 = opt.step(W2, G, M2, step)
+        torch.cuda.synchronize()
+    assert rho == rho2 == po.refresh_indicator(step, WL.K)
+    for a, b in zip(W + M, W2 + M2):
+        assert torch.equal(a, b), "timed step differs from the debug step"
+    out = {i: (pc.to_host(W[i]), pc.to_host(M[i]), pc.to_host(D[i])) for i in sample}
+    del W, M, G, W2, M2, D
+    torch.cuda.empty_cache()
+    return cfg, host_in, out
+
+
+def oriented_rows(A, m, n, rows):
+    return A[rows] if m <= n else A[:, rows].T
+
+
+def check_rows(cfg, i, rows, Do_rows, host_in, out, tol):
+    m, n = WL.shapes[i]
+    W0, M0, G = host_in[i]
+    Wg, Mg, Dg = out[i]
+    oc = pc.oracle_config(cfg)
+    Mo = po.momentum_update(M0, G, oc.beta)
+    Dg_rows = oriented_rows(Dg, m, n, rows)
+    err = pc.rel(Dg_rows, Do_rows)
+    print(f"  {i} {m}x{n}: D rows err {err:.3e}", flush=True)
+    assert err <= tol, f"matrix {i} {m}x{n}: D err {err:.3e} > {tol}"
+    assert pc.rel(oriented_rows(Mg, m, n, rows), oriented_rows(Mo, m, n, rows)) <= pc.TOL_M
+    Wo_rows = (1 - oc.lr * oc.wd) * oriented_rows(W0, m, n, rows) - oc.lr * Do_rows
+    slack = pc.bf16_write_bound(oriented_rows(Wg, m, n, rows), Wo_rows, Dg_rows, Do_rows, cfg.lr)
+    assert slack <= 1.0, f"matrix {i}: W outside the rounding bound ({slack:.3f})"
+
+
+def test_dit4b_refresh_step_sampled_rows():
+    sample = list(range(5))                       # block 0: qkv, out, mlp up, mlp down, adaLN
+    cfg, host_in, out = run(0, sample)
+    oc = pc.oracle_config(cfg)
+    rng = np.random.default_rng(7)
+    for i in sample:
+        m, n = WL.shapes[i]
+        W0, M0, G = host_in[i]
+        U = po.momentum_update(M0, G, oc.beta)
+        X = po.orient(U)
+        rows = np.sort(rng.choice(X.shape[0], 48, replace=False))
+        Do = po.shape_scale(m, n, oc.scale_mode) * po.ns5_rows_closed_form(X, rows, oc.eps_ns, oc.coeffs)
+        check_rows(cfg, i, rows, Do, host_in, out, pc.TOL_NS5)
+
+
+def test_dit4b_rowwise_step_sampled_rows():
+    L = WL.blocks
+    sample = list(range(5)) + list(range(5 * (L - 1), 5 * L))   # first and last block
+    cfg, host_in, out = run(1, sample)
+    oc = pc.oracle_config(cfg)
+    rng = np.random.default_rng(8)
+    for i in sample:
+        m, n = WL.shapes[i]
+        W0, M0, G = host_in[i]
+        U = po.momentum_update(M0, G, oc.beta)
+        r = min(m, n)
+        rows = np.sort(rng.choice(r, 64, replace=False))
+        Xr = oriented_rows(U, m, n, rows)
+        Do = po.shape_scale(m, n, oc.scale_mode) * oc.gamma * po.rownorm(Xr, oc.eps_rownorm)
+        check_rows(cfg, i, rows, Do, host_in, out, pc.TOL_ROWWISE)
