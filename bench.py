@@ -77,6 +77,26 @@ def copy_probe():
                                      "GB_s": gbs, "frac_of_spec": gbs / PEAK_HBM_GBS}}), flush=True)
 
 
+def kernel_source_hash() -> str:
+    import hashlib
+    d = os.path.join(ROOT, "paper_2608_20818_amd", "csrc")
+    src = b"".join(open(os.path.join(d, n), "rb").read() for n in sorted(os.listdir(d)))
+    return hashlib.sha256(src).hexdigest()[:16]
+
+
+def counter_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    passes (calibrated on a plain copy), if they were taken on these kernel
+    sources and this workload; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload.replace('-', '')}.json")
+    if not os.path.exists(path):
+        return None
+    t = json.load(open(path))
+    if t.get("kernel_source_sha256_16") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    return t["classes"]
+
+
 def make_inputs(wl_idx, wl, device):
     import torch
     import synth
@@ -95,10 +115,12 @@ def make_inputs(wl_idx, wl, device):
     return W, M, G
 
 
-def cpu_baseline(wl_idx, wl, K, cfg_vals):
-    """Time the fp64 oracle on a bounded sample of the workload and scale it to
-    one optimizer step of the whole weight set."""
-    import numpy as np
+def cpu_baseline(wl_idx, wl, K, cfg_vals, budget_s: float = 12.0):
+    """Time the fp64 oracle on a bounded sample of the workload (about
+    `budget_s` of host work) and scale it to one optimizer step of the whole
+    weight set: refresh steps on whole matrices of the distinct shapes, cheapest
+    first, scaled by NS5 FLOPs; row-wise steps on 256 full oriented rows of every
+    distinct shape, scaled by elements."""
     import synth
     from oracle import prm_oracle as po
     try:
@@ -108,45 +130,48 @@ def cpu_baseline(wl_idx, wl, K, cfg_vals):
     except Exception:  # pragma: no cover - threadpoolctl is optional
         threads = os.cpu_count() or 1
     oc = po.PRMConfig(K=K, **cfg_vals)
-    shapes = wl.shapes
-    # NS5 sample: the matrix with the fewest NS5 FLOPs (cheapest representative)
-    flops = [po.ns5_flops(m, n) for m, n in shapes]
-    i_ns = min(range(len(shapes)), key=lambda i: flops[i])
-    # row-wise sample: 256 full oriented rows of the longest wide matrix and of a
-    # tall matrix (the oracle's per-element cost does not depend on the row count)
-    i_wide = max((i for i, (m, n) in enumerate(shapes) if m <= n), key=lambda i: shapes[i][1])
-    i_tall = next((i for i, (m, n) in enumerate(shapes) if m > n), None)
-    rw_shapes = [(min(256, shapes[i_wide][0]), shapes[i_wide][1])]
-    if i_tall is not None:
-        rw_shapes.append((shapes[i_tall][0], min(256, shapes[i_tall][1])))
-    m, n = shapes[i_ns]
-    w, mm, g = synth.host_matrix(wl_idx, i_ns, m, n, synth.rank_of(wl, m, n), param_dtype=wl.param_dtype,
-                                 grad_dtype=wl.grad_dtype, beta=wl.beta, steps=(0,))
-    t0 = time.perf_counter()
-    po.step_matrix(w, mm, g[0], 0, oc)
-    t_ns = time.perf_counter() - t0
-    rw_elems, t_rw = 0, 0.0
-    for j, (m, n) in enumerate(rw_shapes):
-        w, mm, g = synth.host_matrix(wl_idx, 10_000 + j, m, n, synth.rank_of(wl, m, n),
+    shapes = list(wl.shapes)
+    distinct = sorted(set(shapes), key=lambda s: po.ns5_flops(*s))
+    first = {s: shapes.index(s) for s in distinct}
+    # row-wise: 256 oriented rows of each distinct shape
+    t_rw, rw_elems, rw_desc = 0.0, 0, []
+    for j, (m, n) in enumerate(distinct):
+        sm, sn = (min(256, m), n) if m <= n else (m, min(256, n))
+        w, mm, g = synth.host_matrix(wl_idx, 10_000 + j, sm, sn, synth.rank_of(wl, sm, sn),
                                      param_dtype=wl.param_dtype, grad_dtype=wl.grad_dtype,
                                      beta=wl.beta, steps=(1,))
         t0 = time.perf_counter()
         po.step_matrix(w, mm, g[1], 1, oc)
         t_rw += time.perf_counter() - t0
-        rw_elems += m * n
-    total_flops = sum(flops)
+        rw_elems += sm * sn
+        rw_desc.append(f"{sm}x{sn}")
+    # refresh: whole matrices, cheapest shapes first, until the budget is spent
+    t_ns, ns_flops, ns_desc = 0.0, 0, []
+    for (m, n) in distinct:
+        i = first[(m, n)]
+        w, mm, g = synth.host_matrix(wl_idx, i, m, n, synth.rank_of(wl, m, n), param_dtype=wl.param_dtype,
+                                     grad_dtype=wl.grad_dtype, beta=wl.beta, steps=(0,))
+        t0 = time.perf_counter()
+        po.step_matrix(w, mm, g[0], 0, oc)
+        dt = time.perf_counter() - t0
+        t_ns += dt
+        ns_flops += po.ns5_flops(m, n)
+        ns_desc.append(f"{m}x{n} ({dt:.1f}s)")
+        if t_ns + t_rw >= budget_s:
+            break
+    total_flops = sum(po.ns5_flops(m, n) for m, n in shapes)
     total_elems = sum(m * n for m, n in shapes)
-    T_ref = t_ns * total_flops / flops[i_ns] * 1e3
+    T_ref = t_ns / ns_flops * total_flops * 1e3
     T_rw = t_rw / rw_elems * total_elems * 1e3
     amort = (T_ref + (K - 1) * T_rw) / K
     return {
         "value": amort, "unit": "ms", "cores": int(threads), "kind": "oracle",
         "host_cpus": os.cpu_count(),
-        "refresh_ms": T_ref, "rowwise_ms": T_rw,
-        "sample": (f"fp64 NumPy oracle: one refresh step of matrix {shapes[i_ns]} ({t_ns:.1f}s) scaled by "
-                   f"NS5 FLOPs (x{total_flops / flops[i_ns]:.1f}); one row-wise step of "
-                   f"{' and '.join(str(s) for s in rw_shapes)} (full oriented rows, {t_rw:.2f}s) scaled "
-                   f"by elements (x{total_elems / rw_elems:.1f}); amortized over K={K}"),
+        "refresh_ms": T_ref, "rowwise_ms": T_rw, "sample_seconds": t_ns + t_rw,
+        "sample": (f"fp64 NumPy oracle: refresh steps of whole matrices {', '.join(ns_desc)} scaled by NS5 "
+                   f"FLOPs (x{total_flops / ns_flops:.1f}); row-wise steps of 256 full oriented rows of "
+                   f"{', '.join(rw_desc)} ({t_rw:.2f}s) scaled by elements (x{total_elems / rw_elems:.1f}); "
+                   f"amortized over K={K}"),
     }
 
 
@@ -258,6 +283,12 @@ def main():
         if rw_names:
             dom_rw = max(rw_names, key=lambda k: kernels[k]["total_ms"])
             roofline_rw = roof(dom_rw, kernels[dom_rw])
+        traffic = counter_traffic(wl.name)
+        for rf in (roofline, roofline_rw):
+            if rf is not None and traffic and rf["kernel"] in traffic:
+                tc = traffic[rf["kernel"]]
+                rf["traffic"] = tc["fetch_bytes_per_launch"] + tc["write_bytes_per_launch"]
+                rf["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
         log(f"[bench] kernels: " + ", ".join(f"{k} {v['total_ms']:.2f}ms/{v['launches']}" for k, v in kernels.items() if v["launches"]))
 
     opt.close()
@@ -292,6 +323,9 @@ def main():
         "rowwise_ms": T_rw,
         "refresh_mfma_frac": refresh_mfma_frac,
         "rowwise_hbm_frac": rowwise_hbm_frac,
+        "amortized_ms_by_K": ({str(k): (T_ref + (k - 1) * T_rw) / k for k in (1, 3, 5, 10)}
+                              if ref and rw else None),
+        "single_gpu_reduction_K3_vs_K1": ((T_ref - (T_ref + 2 * T_rw) / 3) / T_ref if ref and rw else None),
         "refresh_alg_tflop": ns_flops / 1e12,
         "rowwise_alg_gb": rw_bytes / 1e9,
         "roofline": roofline,

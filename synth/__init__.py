@@ -15,9 +15,10 @@ momenta with the shapes and value distributions of the workloads:
   it is drawn directly from that distribution (one seeded draw).
 
 Seeds: numpy.random.SeedSequence([20818, workload, matrix, tag]).  Host draws
-use PCG64; device draws (large workloads) seed a torch generator on the GPU
-from the same sequence, and any matrix the oracle needs is copied back from
-the device so that both sides read identical bytes.
+use PCG64.  Device draws (large workloads) take the thin Haar factors from the
+host draw and the large Gaussian terms from a torch generator on the GPU seeded
+from the same sequence; any matrix the oracle needs is copied back from the
+device so that both sides read identical bytes.
 """
 from __future__ import annotations
 
@@ -183,19 +184,15 @@ def device_matrix(workload: int, mat: int, m: int, n: int, k: int, *, param_dtyp
         g.manual_seed(torch_seed(workload, mat, tag, t))
         return g
 
-    def haar(tag, rows):
-        Z = torch.randn(rows, k, generator=gen(tag), device=device, dtype=torch.float32)
-        Q, R = torch.linalg.qr(Z)
-        d = torch.sign(torch.diagonal(R))
-        d[d == 0] = 1.0
-        return Q * d
-
     out = {}
     if "W" in want:
         out["W"] = (0.02 * torch.randn(m, n, generator=gen("W"), device=device)).to(dt[param_dtype])
     if "M" in want or "G" in want:
-        U = haar("U", m)
-        V = haar("V", n)
+        # the thin Haar factors are small (m x k, n x k): drawn on the host with
+        # the same seeds as host_matrix, so both paths share U and V exactly
+        Uh, Vh = host_factors(workload, mat, m, n, k)
+        U = torch.tensor(Uh, dtype=torch.float32, device=device)
+        V = torch.tensor(Vh, dtype=torch.float32, device=device)
         s = 1.0 / torch.arange(1, k + 1, device=device, dtype=torch.float32)
         if "M" in want:
             sig_m = 1.0 + beta + beta * beta
