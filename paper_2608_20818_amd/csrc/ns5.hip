@@ -5,26 +5,27 @@
 // five times from X_0 = U~ / (||U~||_F + eps_ns), then the parameter write of
 // eq. (periodic-direction) with the oriented result mapped back.
 //
-// Kernels, all batched over the matrices of a workspace chunk through work
-// item lists (matrix, tile row, tile column):
-//  * ns_prologue: momentum update, per-tile sum of squares, bf16(U) written
-//    both in the oriented layout X (r x c) and transposed XT (c x r), through
-//    an LDS tile transpose.  The Frobenius scale is not applied here: NS5 is
-//    homogeneous, so alpha = 1/(||U||+eps) is folded into the first Gram
-//    (alpha^2) and the first apply (alpha) epilogues.
+// Only the transposed iterate XT = X^T (c x r, row-major) is kept.  Kernels,
+// all batched over the matrices of a workspace chunk through work item lists
+// (matrix, tile row, tile column):
+//  * ns_prologue: momentum update, per-tile sum of squares, bf16(U~^T) written
+//    as XT (through an LDS tile transpose for wide matrices).  The Frobenius
+//    scale is not applied here: NS5 is homogeneous, so alpha = 1/(||U||+eps) is
+//    folded into the first Gram (alpha^2) and the first apply (alpha).
 //  * ns_alpha: fixed-order reduction of the tile sums into alpha.
-//  * ns_gemm: C = P Q^T on bf16 operands with fp32 MFMA accumulation
-//    (v_mfma_f32_32x32x16_bf16), 256 x 256 tiles, BK = 64, operands streamed
-//    into a double LDS buffer by direct global-to-LDS loads.  Every product of the iteration has this NT form:
-//      Gram   A   = X X^T              (upper tiles only, mirrored)
-//      square A^2 = A A^T              (A is symmetric; upper tiles, mirrored)
-//      apply  B X = B (XT)^T           (XT is the transposed copy of X)
+//  * ns_gemm: bf16 MFMA products (v_mfma_f32_32x32x16_bf16) with fp32
+//    accumulation on 256 x 256 tiles, K in stages of 64 streamed into a double
+//    LDS buffer by direct global-to-LDS loads:
+//      Gram   A   = X X^T = XT^T XT    K-major operands ("TN"), read from LDS
+//                                      with transposing ds_read_b64_tr_b16;
+//                                      upper tiles only, mirrored
+//      square A^2 = A A^T              (A is symmetric) upper tiles, mirrored
+//      apply  X'^T = XT (aI + dB) + XT Bo    ("NT"; Bo is symmetric)
 //    The diagonals of A and B are the large entries, so they are carried in
 //    fp32 and only the off-diagonal parts Ao, Bo are rounded to bf16 for the
-//    next product:  A^2 = dA^2 + dA Ao + Ao dA + Ao Ao  and
-//    X' = (a I + dB) X + Bo X, with the diagonal products applied in the
-//    epilogues.  Epilogues also fold alpha, and at the last iteration perform
-//    the parameter write W <- (1 - eta lambda) W - eta s O^{-1}(X_5).
+//    next product:  A^2 = dA^2 + dA Ao + Ao dA + Ao Ao, with the diagonal terms
+//    applied in the epilogues.  Epilogues also fold alpha, and at the last
+//    iteration perform the parameter write W <- (1 - eta lambda) W - eta s O^{-1}(X_5).
 // The workspace is padded to whole tiles and the padding stays exactly zero
 // through every iteration, so the GEMMs need no bounds checks.
 #include <type_traits>
@@ -54,11 +55,11 @@ __global__ __launch_bounds__(256) void ns_prologue_kernel(const MatDesc* __restr
   const Item it = items[blockIdx.x];
   const MatDesc& d = md[it.mat];
   const int64_t m = d.m, n = d.n;
-  // natural = stored orientation (X for wide, XT for tall); other = transposed
-  uint16_t* nat = d.tall ? d.XT : d.X;
-  uint16_t* tra = d.tall ? d.X : d.XT;
-  const int64_t ldn = d.tall ? d.rp : d.cp;
-  const int64_t ldt = d.tall ? d.cp : d.rp;
+  // XT (cp x rp) is the stored layout of a tall matrix and the transpose of a
+  // wide one
+  uint16_t* XT = d.XT;
+  const int64_t ld = d.rp;
+  const bool tall = d.tall;
   const int64_t R0 = (int64_t)it.tm * T, C0 = (int64_t)it.tn * T;
   const int tc = (threadIdx.x & 15) * 4;
   const int tr = threadIdx.x >> 4;
@@ -96,20 +97,25 @@ __global__ __launch_bounds__(256) void ns_prologue_kernel(const MatDesc* __restr
 #pragma unroll
     for (int k = 0; k < 4; ++k) ss += u[k] * u[k];
     const uint32_t h0 = f2bf(u[0]), h1 = f2bf(u[1]), h2 = f2bf(u[2]), h3 = f2bf(u[3]);
-    *reinterpret_cast<uint2*>(nat + row * ldn + col) = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
-    tile[r][tc + 0] = (uint16_t)h0;
-    tile[r][tc + 1] = (uint16_t)h1;
-    tile[r][tc + 2] = (uint16_t)h2;
-    tile[r][tc + 3] = (uint16_t)h3;
+    if (tall) {
+      *reinterpret_cast<uint2*>(XT + row * ld + col) = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
+    } else {
+      tile[r][tc + 0] = (uint16_t)h0;
+      tile[r][tc + 1] = (uint16_t)h1;
+      tile[r][tc + 2] = (uint16_t)h2;
+      tile[r][tc + 3] = (uint16_t)h3;
+    }
   }
-  __syncthreads();
+  if (!tall) {  // uniform per work group
+    __syncthreads();
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int j = tr + 16 * i;  // tile column -> transposed row
-    const uint32_t v0 = tile[tc + 0][j], v1 = tile[tc + 1][j], v2 = tile[tc + 2][j],
-                   v3 = tile[tc + 3][j];
-    *reinterpret_cast<uint2*>(tra + (C0 + j) * ldt + R0 + tc) =
-        make_uint2(v0 | (v1 << 16), v2 | (v3 << 16));
+    for (int i = 0; i < 4; ++i) {
+      const int j = tr + 16 * i;  // tile column -> transposed row
+      const uint32_t v0 = tile[tc + 0][j], v1 = tile[tc + 1][j], v2 = tile[tc + 2][j],
+                     v3 = tile[tc + 3][j];
+      *reinterpret_cast<uint2*>(XT + (C0 + j) * ld + R0 + tc) =
+          make_uint2(v0 | (v1 << 16), v2 | (v3 << 16));
+    }
   }
   ss = block_sum<256>(ss, red);
   if (threadIdx.x == 0) d.partial[(int64_t)it.tm * d.ptiles_n + it.tn] = ss;
@@ -162,6 +168,14 @@ typedef __attribute__((address_space(3))) void* lds_ptr;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(1))) u32x4* gptr4;
 
+// K-major ("TN") stage tile: 64 k-rows of 256 bf16 (512 B, 32 chunks of 16 B);
+// chunk c of row r is stored at c ^ (r % 16).
+constexpr int TN_ROW_BYTES = BM * 2;
+__device__ __forceinline__ int swz_tn(int r, int ch) { return r * TN_ROW_BYTES + ((ch ^ (r & 15)) << 4); }
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16* lds_v4i16;
+
 // fp32 staging tile of the epilogue (QM x 256, no padding): column c of row r
 // is stored at c ^ (8 * ((r / 8) % 8)), which keeps aligned 8-column groups
 // contiguous (row-major pass) and makes the column pass, where 8 lanes read 8
@@ -184,34 +198,52 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const bool even = (p.iter & 1) == 0;
-  const uint16_t* Xc = even ? d.X : d.Xn;
   const uint16_t* XTc = even ? d.XT : d.XTn;
-  uint16_t* Xo = even ? d.Xn : d.X;
   uint16_t* XTo = even ? d.XTn : d.XT;
   const int64_t rp = d.rp, cp = d.cp;
 
+  // C[row][col] = sum_k P[row][k] Q[col][k]   (NT), or
+  // C[row][col] = sum_k P[k][row] Q[k][col]   (TN, the Gram on XT)
+  constexpr bool TN = (KIND == GEMM_GRAM);
   const uint16_t *P, *Q;
-  int64_t ld;
+  const int64_t ld = rp;  // every operand has rp columns
+  int64_t klen;
   if constexpr (KIND == GEMM_GRAM) {
-    P = Xc; Q = Xc; ld = cp;
+    P = XTc; Q = XTc; klen = cp;
   } else if constexpr (KIND == GEMM_POLY) {
-    P = d.Ao; Q = d.Ao; ld = rp;
+    P = d.Ao; Q = d.Ao; klen = rp;
   } else {
-    P = d.Bo; Q = XTc; ld = rp;
+    P = XTc; Q = d.Bo; klen = rp;   // X'^T tile: rows of XT, columns of Bo
   }
   const int64_t row0 = (int64_t)it.tm * BM, col0 = (int64_t)it.tn * BN;
-  const int nk = (int)(ld / BK);  // even: the padded contraction length is a multiple of the tile
+  const int nk = (int)(klen / BK);  // a multiple of 4: the padded dimensions are multiples of the tile
 
-  // DMA sources: wave instruction q covers tile rows 64 wave + 8 q + lane / 8;
+  // DMA sources.  NT: wave load q covers tile rows 64 wave + 8 q + lane / 8 and
   // lane fills physical chunk lane % 8, i.e. logical chunk (lane % 8) ^ (row % 8).
-  const int64_t lane_off = (int64_t)(lane >> 3) * ld + (((lane & 7) ^ (lane >> 3)) << 3);
-  const uint16_t* srcA = P + (row0 + 64 * wave) * ld + lane_off;
-  const uint16_t* srcB = Q + (col0 + 64 * wave) * ld + lane_off;
-  // One 1 KB wave load of the stage: block q < 8 of operand A, q >= 8 of B.
+  // TN: wave load q covers k-rows 16 wave + 2 q + lane / 32 and lane fills
+  // physical chunk lane % 32, i.e. logical chunk (lane % 32) ^ (k-row % 16).
+  const uint16_t *srcA, *srcB;
+  if constexpr (TN) {
+    srcA = P + (int64_t)(16 * wave + (lane >> 5)) * ld + row0;
+    srcB = Q + (int64_t)(16 * wave + (lane >> 5)) * ld + col0;
+  } else {
+    const int64_t lane_off = (int64_t)(lane >> 3) * ld + (((lane & 7) ^ (lane >> 3)) << 3);
+    srcA = P + (row0 + 64 * wave) * ld + lane_off;
+    srcB = Q + (col0 + 64 * wave) * ld + lane_off;
+  }
+  // One 1 KB wave load of the stage at k offset `k`: block q < 8 of operand A,
+  // q >= 8 of operand B.
   auto dma1 = [&](char* stage, int64_t k, int q) {
     const bool isb = q >= DMA_PER_WAVE;
     const int qq = isb ? q - DMA_PER_WAVE : q;
-    __builtin_amdgcn_global_load_lds((const void*)((isb ? srcB : srcA) + (int64_t)(8 * qq) * ld + k),
+    const uint16_t* src;
+    if constexpr (TN) {
+      const int krow = 2 * qq + (lane >> 5);  // + 16 wave, which is 0 mod 16
+      src = (isb ? srcB : srcA) + (k + 2 * qq) * ld + ((((lane & 31) ^ (krow & 15))) << 3);
+    } else {
+      src = (isb ? srcB : srcA) + (int64_t)(8 * qq) * ld + k;
+    }
+    __builtin_amdgcn_global_load_lds((const void*)src,
                                      (lds_ptr)(stage + (isb ? A_BYTES : 0) + (DMA_PER_WAVE * wave + qq) * 1024),
                                      16, 0, 0);
   };
@@ -227,6 +259,22 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
 
   const int arow = wm * WM + (lane & 31), brow = wn * WN + (lane & 31);
   const int khalf = lane >> 5;
+  // TN fragment addresses (k-step 0): lane L of 16-lane group g = L / 16 reads
+  // k-row 8 (g / 2) + 4 kk + (L % 16) / 4 at columns m0 + 16 (g % 2) + 4 (L % 4)
+  int tn_off[MI][2], tn_offb[MI][2];
+  if constexpr (TN) {
+    const int g = lane >> 4, jl = lane & 15;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int kr = 8 * (g >> 1) + 4 * kk + (jl >> 2);
+        const int ma = wm * WM + i * 32 + 16 * (g & 1) + 4 * (jl & 3);
+        const int mb = wn * WN + i * 32 + 16 * (g & 1) + 4 * (jl & 3);
+        tn_off[i][kk] = swz_tn(kr, ma >> 3) + ((ma & 7) << 1);
+        tn_offb[i][kk] = swz_tn(kr, mb >> 3) + ((mb & 7) << 1);
+      }
+  }
 
   // Compute one stage from `cur` while streaming stage `knext` (if >= 0) into
   // `nxt`.  The vector-memory path accepts about one 1 KB wave load per 16
@@ -241,9 +289,20 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
     const bool more = knext >= 0;
     bf16x8 fa[2][MI], fb[2][NI];
     auto rd = [&](int set, int i, int ks) {
-      const int ch = ks * 2 + khalf;
-      fa[set][i] = *reinterpret_cast<const bf16x8*>(a + swz(arow + i * 32, ch));
-      fb[set][i] = *reinterpret_cast<const bf16x8*>(b + swz(brow + i * 32, ch));
+      if constexpr (TN) {
+        // two transposing reads give lane L the column (L % 32) of the block
+        // at 8 consecutive k: k-rows 16 ks + 8 (L / 32) + 4 kk + s, s = 0..3
+        v4i16 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(a + tn_off[i][0] + ks * 16 * TN_ROW_BYTES));
+        v4i16 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(a + tn_off[i][1] + ks * 16 * TN_ROW_BYTES));
+        v4i16 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(b + tn_offb[i][0] + ks * 16 * TN_ROW_BYTES));
+        v4i16 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(b + tn_offb[i][1] + ks * 16 * TN_ROW_BYTES));
+        fa[set][i] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+        fb[set][i] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7));
+      } else {
+        const int ch = ks * 2 + khalf;
+        fa[set][i] = *reinterpret_cast<const bf16x8*>(a + swz(arow + i * 32, ch));
+        fb[set][i] = *reinterpret_cast<const bf16x8*>(b + swz(brow + i * 32, ch));
+      }
     };
     if (more) {
 #pragma unroll
@@ -285,7 +344,9 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   const bool diag = sym && it.tm == it.tn;
   const bool last = (KIND == GEMM_APPLY) && p.last;
   const float alpha = (p.iter == 0) ? *d.alpha : 1.0f;
-  const bool need_t = (sym && !diag) || (KIND == GEMM_APPLY && (!last || d.tall));
+  // transposed outputs: Gram/square mirror tiles, and the parameter write of a
+  // wide matrix (the apply tile is a tile of X^T)
+  const bool need_t = (sym && !diag) || (last && !d.tall);
 
   // Epilogue in four quarters of QM rows, staged alternately in s0 and s1.
   constexpr int EPR = 8;                    // consecutive elements per thread
@@ -318,14 +379,13 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
       else stage_acc(T, std::integral_constant<int, 0>{});
     }
     const int64_t qrow0 = row0 + h * QM;
-    // inputs of the natural-layout pass (X for apply, Ao for the square)
+    // inputs of the natural-layout pass (XT for apply, Ao for the square)
     u32x4 xin[NPASS];  // packed bf16
     if constexpr (KIND != GEMM_GRAM) {
-      const uint16_t* src = (KIND == GEMM_APPLY) ? Xc : d.Ao;
-      const int64_t lds_ = (KIND == GEMM_APPLY) ? cp : rp;
+      const uint16_t* src = (KIND == GEMM_APPLY) ? XTc : d.Ao;
 #pragma unroll
       for (int ps = 0; ps < NPASS; ++ps)
-        xin[ps] = *(gptr4)(src + (qrow0 + ps * RPP + er) * lds_ + col0 + ec);
+        xin[ps] = *(gptr4)(src + (qrow0 + ps * RPP + er) * rp + col0 + ec);
     }
     auto xval = [&](int ps, int q) {
       const uint32_t w = xin[ps][q >> 1];
@@ -368,14 +428,15 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
         }
         Vec<uint16_t>::store8(d.Bo + gi * rp + gj, v);
       } else {
-        // X' = alpha ((a + dB_i) X + Bo X)
-        const float ai = p.a + d.dB[gi];
+        // X'^T[gi][gj] = alpha ((a + dB[gj]) XT[gi][gj] + (XT Bo)[gi][gj])
+        float db[EPR];
+        Vec<float>::load8(d.dB + gj, db);
 #pragma unroll
-        for (int q = 0; q < EPR; ++q) v[q] = alpha * (ai * xval(ps, q) + v[q]);
+        for (int q = 0; q < EPR; ++q) v[q] = alpha * ((p.a + db[q]) * xval(ps, q) + v[q]);
         if (!last) {
-          Vec<uint16_t>::store8(Xo + gi * cp + gj, v);
-        } else if (!d.tall) {
-          // oriented (gi, gj) is stored (gi, gj): W is r x c = m x n
+          Vec<uint16_t>::store8(XTo + gi * rp + gj, v);
+        } else if (d.tall) {
+          // tall: the tile of X^T is a tile of W (c x r = m x n)
           const int64_t n = d.n;
           if (gi < d.m) {
             const float dc = d.s * p.dscale;
@@ -427,10 +488,8 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
       } else if constexpr (KIND == GEMM_POLY) {
         Vec<uint16_t>::store8(d.Bo + orow * rp + ocol, v);
       } else {
-        if (!last) {
-          Vec<uint16_t>::store8(XTo + orow * rp + ocol, v);
-        } else {
-          // tall: oriented (i, j) is stored (j, i); W is c x r = m x n
+        {
+          // wide: the transposed tile of X^T is a tile of W (r x c = m x n)
           const int64_t n = d.n;
           if (orow < d.m) {
             const float dc = d.s * p.dscale;

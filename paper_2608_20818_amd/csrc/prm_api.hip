@@ -122,12 +122,12 @@ float shape_scale(int64_t m, int64_t n, int mode) {
   }
 }
 
-// NS5 workspace of one matrix: X, XT and the next iterate in both layouts
-// (bf16), off-diagonal A and B (bf16), diagonals of A and B (fp32).
+// NS5 workspace of one matrix: the transposed iterate and the next one (bf16),
+// off-diagonal A and B (bf16), diagonals of A and B (fp32).
 uint64_t ns_matrix_bytes(int64_t rp, int64_t cp) {
   const uint64_t xs = align256((uint64_t)rp * cp * 2), gs = align256((uint64_t)rp * rp * 2),
                  vs = align256((uint64_t)rp * 4);
-  return 4 * xs + 2 * gs + 2 * vs;
+  return 2 * xs + 2 * gs + 2 * vs;
 }
 
 // Row-wise launch class of a wide row of length n (0 tpr = generic path).
@@ -302,7 +302,7 @@ void build_lists(Plan& P, const prm_config* cfg) {
       const int i = ch.mats[k];
       const int32_t tr = (int32_t)(P.rp[i] / kNsTile), tc = (int32_t)(P.cp[i] / kNsTile);
       tile_order(i, tr, tr, true, g[k % kXcds]);
-      tile_order(i, tr, tc, false, a[k % kXcds]);
+      tile_order(i, tc, tr, false, a[k % kXcds]);  // tiles of X'^T: rows over c, columns over r
     }
     ch.gram = interleave_xcd(g);
     ch.poly = ch.gram;
@@ -664,14 +664,12 @@ int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* 
     const uint64_t xs = align256((uint64_t)d.rp * d.cp * 2), gs = align256((uint64_t)d.rp * d.rp * 2),
                    vs = align256((uint64_t)d.rp * 4);
     char* w = chunk_base + P.ws_off[i];
-    d.X = (uint16_t*)w;
-    d.XT = (uint16_t*)(w + xs);
-    d.Xn = (uint16_t*)(w + 2 * xs);
-    d.XTn = (uint16_t*)(w + 3 * xs);
-    d.Ao = (uint16_t*)(w + 4 * xs);
-    d.Bo = (uint16_t*)(w + 4 * xs + gs);
-    d.dA = (float*)(w + 4 * xs + 2 * gs);
-    d.dB = (float*)(w + 4 * xs + 2 * gs + vs);
+    d.XT = (uint16_t*)w;
+    d.XTn = (uint16_t*)(w + xs);
+    d.Ao = (uint16_t*)(w + 2 * xs);
+    d.Bo = (uint16_t*)(w + 2 * xs + gs);
+    d.dA = (float*)(w + 2 * xs + 2 * gs);
+    d.dB = (float*)(w + 2 * xs + 2 * gs + vs);
     d.ptiles_m = (int32_t)((d.tall ? d.cp : d.rp) / kPrologueTile);
     d.ptiles_n = (int32_t)((d.tall ? d.rp : d.cp) / kPrologueTile);
     d.partial = (float*)(small_base + P.small_off[i]);

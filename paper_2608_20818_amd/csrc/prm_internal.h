@@ -21,11 +21,10 @@ struct MatDesc {
   float s;       // shape scale s(W)
   int32_t tall;  // m > n: oriented rows are stored columns
   // NS5 workspace (bf16 bit patterns), valid while this matrix's chunk runs.
-  // Oriented r x c is padded to rp x cp (multiples of the GEMM tile).
-  uint16_t* X;    // rp x cp   iterate, row-major
-  uint16_t* XT;   // cp x rp   its transpose
-  uint16_t* Xn;   // rp x cp   next iterate
-  uint16_t* XTn;  // cp x rp
+  // Oriented r x c is padded to rp x cp (multiples of the GEMM tile); the
+  // iterate is kept transposed, XT = X^T (cp x rp, row-major).
+  uint16_t* XT;   // cp x rp   iterate
+  uint16_t* XTn;  // cp x rp   next iterate
   uint16_t* Ao;   // rp x rp   Gram matrix A = X X^T with its diagonal set to zero (bf16)
   uint16_t* Bo;   // rp x rp   B = b A + c A^2 with its diagonal set to zero (bf16)
   float* dA;      // rp        diagonal of A (fp32)

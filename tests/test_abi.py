@@ -70,10 +70,11 @@ def test_workspace_planning():
     tiny = synth.WORKLOADS[0].shapes
     b = prm.workspace_bytes(tiny, cfg)
     assert b > 0
-    # NS5 region of one matrix: 8 rp cp + 4 rp^2 + 8 rp bytes (X, XT and their
-    # next iterates in bf16, off-diagonal A and B in bf16, their diagonals in fp32)
+    # NS5 region of one matrix: 4 rp cp + 4 rp^2 + 8 rp bytes (the transposed
+    # iterate and the next one in bf16, off-diagonal A and B in bf16, their
+    # diagonals in fp32)
     one = prm.workspace_bytes([(256, 1024)], cfg)
-    assert one >= 8 * 256 * 1024 + 4 * 256 * 256 + 8 * 256
+    assert one >= 4 * 256 * 1024 + 4 * 256 * 256 + 8 * 256
     # a budget smaller than one matrix is refused; a small budget forces chunking
     small = prm.config_default(workspace_budget_bytes=1000)
     with pytest.raises(prm.PRMError) as e:
