@@ -75,18 +75,18 @@ __global__ __launch_bounds__(256) void ns_prologue_kernel(const MatDesc* __restr
     if (row < m) {
       if (vec && col + 3 < n) {
         float g[4], mm[4];
-        Vec<GT>::load4(G + row * n + col, g);
-        Vec<float>::load4(M + row * n + col, mm);
+        VecNT<GT>::load4(G + row * n + col, g);
+        VecNT<float>::load4(M + row * n + col, mm);
 #pragma unroll
         for (int k = 0; k < 4; ++k) mm[k] = p.beta * mm[k] + p.gcoef * g[k];
-        Vec<float>::store4(M + row * n + col, mm);
+        VecNT<float>::store4(M + row * n + col, mm);
 #pragma unroll
         for (int k = 0; k < 4; ++k) u[k] = p.nesterov ? g[k] + p.beta * mm[k] : mm[k];
       } else {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           if (col + k < n) {
-            const float g = Vec<GT>::load1(G + row * n + col + k);
+            const float g = VecNT<GT>::load1(G + row * n + col + k);
             const float mm = p.beta * M[row * n + col + k] + p.gcoef * g;
             M[row * n + col + k] = mm;
             u[k] = p.nesterov ? g + p.beta * mm : mm;

@@ -71,6 +71,67 @@ template <> struct Vec<uint16_t> {
   __device__ __forceinline__ static void store1(uint16_t* p, float v) { *p = (uint16_t)f2bf(v); }
 };
 
+// ---- streaming (nontemporal) variants for data touched once per step ---------
+// Same interface as Vec; the loads and stores carry the nontemporal hint so that
+// the single pass over G, M and W does not displace cached operands.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+
+template <typename T> struct VecNT;
+
+template <> struct VecNT<float> {
+  __device__ __forceinline__ static void load4(const float* p, float v[4]) {
+    const f32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p));
+    v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
+  }
+  __device__ __forceinline__ static void store4(float* p, const float v[4]) {
+    const f32x4_t x = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(x, reinterpret_cast<f32x4_t*>(p));
+  }
+  __device__ __forceinline__ static void load8(const float* p, float v[8]) {
+    load4(p, v);
+    load4(p + 4, v + 4);
+  }
+  __device__ __forceinline__ static void store8(float* p, const float v[8]) {
+    store4(p, v);
+    store4(p + 4, v + 4);
+  }
+  __device__ __forceinline__ static float load1(const float* p) { return __builtin_nontemporal_load(p); }
+  __device__ __forceinline__ static void store1(float* p, float v) { __builtin_nontemporal_store(v, p); }
+};
+
+template <> struct VecNT<uint16_t> {
+  __device__ __forceinline__ static void load4(const uint16_t* p, float v[4]) {
+    const u32x2_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+    v[0] = bf2f(x[0] & 0xffffu); v[1] = bf2f(x[0] >> 16);
+    v[2] = bf2f(x[1] & 0xffffu); v[3] = bf2f(x[1] >> 16);
+  }
+  __device__ __forceinline__ static void store4(uint16_t* p, const float v[4]) {
+    const u32x2_t x = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
+    __builtin_nontemporal_store(x, reinterpret_cast<u32x2_t*>(p));
+  }
+  __device__ __forceinline__ static void load8(const uint16_t* p, float v[8]) {
+    const u32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      v[2 * k] = bf2f(x[k] & 0xffffu);
+      v[2 * k + 1] = bf2f(x[k] >> 16);
+    }
+  }
+  __device__ __forceinline__ static void store8(uint16_t* p, const float v[8]) {
+    const u32x4_t x = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]),
+                       pack_bf2(v[6], v[7])};
+    __builtin_nontemporal_store(x, reinterpret_cast<u32x4_t*>(p));
+  }
+  __device__ __forceinline__ static float load1(const uint16_t* p) {
+    return bf2f(__builtin_nontemporal_load(p));
+  }
+  __device__ __forceinline__ static void store1(uint16_t* p, float v) {
+    __builtin_nontemporal_store((uint16_t)f2bf(v), p);
+  }
+};
+
 // ---- reductions (fixed order: deterministic run to run) ---------------------
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

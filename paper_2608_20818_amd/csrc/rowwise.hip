@@ -81,9 +81,9 @@ __global__ __launch_bounds__(NT) void rw_wide_kernel(const MatDesc* __restrict__
     const int64_t e = (int64_t)(it * TPR + lt) * 8;
     ok[it] = row_ok && e < n;
     if (ok[it]) {
-      Vec<GT>::load8(G + e, g[it]);
-      Vec<float>::load8(M + e, u[it]);
-      Vec<WT>::load8(W + e, w[it]);
+      VecNT<GT>::load8(G + e, g[it]);
+      VecNT<float>::load8(M + e, u[it]);
+      VecNT<WT>::load8(W + e, w[it]);
     }
   }
   float ss = 0.f;
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(NT) void rw_wide_kernel(const MatDesc* __restrict__
       const int64_t e = (int64_t)(it * TPR + lt) * 8;
 #pragma unroll
       for (int k = 0; k < 8; ++k) u[it][k] = p.beta * u[it][k] + p.gcoef * g[it][k];
-      Vec<float>::store8(M + e, u[it]);
+      VecNT<float>::store8(M + e, u[it]);
       if (p.nesterov) {
 #pragma unroll
         for (int k = 0; k < 8; ++k) u[it][k] = g[it][k] + p.beta * u[it][k];
@@ -116,8 +116,8 @@ __global__ __launch_bounds__(NT) void rw_wide_kernel(const MatDesc* __restrict__
         dv[k] = u[it][k] * kcoef;
         w[it][k] = w[it][k] * p.decay - p.lr * dv[k];
       }
-      Vec<WT>::store8(W + e, w[it]);
-      if (p.write_d) Vec<float>::store8(Dp + e, dv);
+      VecNT<WT>::store8(W + e, w[it]);
+      if (p.write_d) VecNT<float>::store8(Dp + e, dv);
     }
   }
 }
@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256) void rw_generic_kernel(const MatDesc* __restri
   WT* W = reinterpret_cast<WT*>(d.W) + row * n;
   float ss = 0.f;
   for (int64_t e = threadIdx.x; e < n; e += 256) {
-    const float g = Vec<GT>::load1(G + e);
+    const float g = VecNT<GT>::load1(G + e);
     float m = p.beta * M[e] + p.gcoef * g;
     M[e] = m;
     const float u = p.nesterov ? g + p.beta * m : m;
@@ -156,9 +156,9 @@ __global__ __launch_bounds__(256) void rw_generic_kernel(const MatDesc* __restri
   float* Dp = d.D + row * n;
   for (int64_t e = threadIdx.x; e < n; e += 256) {
     const float m = M[e];
-    const float u = p.nesterov ? Vec<GT>::load1(G + e) + p.beta * m : m;
+    const float u = p.nesterov ? VecNT<GT>::load1(G + e) + p.beta * m : m;
     const float dv = u * kcoef;
-    Vec<WT>::store1(W + e, Vec<WT>::load1(W + e) * p.decay - p.lr * dv);
+    VecNT<WT>::store1(W + e, VecNT<WT>::load1(W + e) * p.decay - p.lr * dv);
     if (p.write_d) Dp[e] = dv;
   }
 }
@@ -192,10 +192,10 @@ __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __res
       for (int q = 0; q < UNR; ++q) {
         const int64_t off = (r + q) * n + col;
         if constexpr (VEC == 4) {
-          Vec<GT>::load4(G + off, g[q]);
-          Vec<float>::load4(M + off, m[q]);
+          VecNT<GT>::load4(G + off, g[q]);
+          VecNT<float>::load4(M + off, m[q]);
         } else {
-          g[q][0] = Vec<GT>::load1(G + off);
+          g[q][0] = VecNT<GT>::load1(G + off);
           m[q][0] = M[off];
         }
       }
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __res
         const int64_t off = (r + q) * n + col;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) m[q][k] = p.beta * m[q][k] + p.gcoef * g[q][k];
-        if constexpr (VEC == 4) Vec<float>::store4(M + off, m[q]); else M[off] = m[q][0];
+        if constexpr (VEC == 4) VecNT<float>::store4(M + off, m[q]); else M[off] = m[q][0];
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
           const float u = p.nesterov ? g[q][k] + p.beta * m[q][k] : m[q][k];
@@ -216,15 +216,15 @@ __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __res
       const int64_t off = r * n + col;
       float g[VEC], m[VEC];
       if constexpr (VEC == 4) {
-        Vec<GT>::load4(G + off, g);
-        Vec<float>::load4(M + off, m);
+        VecNT<GT>::load4(G + off, g);
+        VecNT<float>::load4(M + off, m);
       } else {
-        g[0] = Vec<GT>::load1(G + off);
+        g[0] = VecNT<GT>::load1(G + off);
         m[0] = M[off];
       }
 #pragma unroll
       for (int k = 0; k < VEC; ++k) m[k] = p.beta * m[k] + p.gcoef * g[k];
-      if constexpr (VEC == 4) Vec<float>::store4(M + off, m); else M[off] = m[0];
+      if constexpr (VEC == 4) VecNT<float>::store4(M + off, m); else M[off] = m[0];
 #pragma unroll
       for (int k = 0; k < VEC; ++k) {
         const float u = p.nesterov ? g[k] + p.beta * m[k] : m[k];
@@ -232,7 +232,7 @@ __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __res
       }
     }
     float* cp = d.colpart + (int64_t)it.tm * n + col;
-    if constexpr (VEC == 4) Vec<float>::store4(cp, acc); else cp[0] = acc[0];
+    if constexpr (VEC == 4) VecNT<float>::store4(cp, acc); else cp[0] = acc[0];
   }
 }
 
@@ -279,13 +279,13 @@ __global__ __launch_bounds__(256) void rw_tall_apply_kernel(const MatDesc* __res
       if (r + q < r1) {
         const int64_t off = (r + q) * n + col;
         if constexpr (VEC == 4) {
-          Vec<float>::load4(M + off, m[q]);
-          Vec<WT>::load4(W + off, w[q]);
-          if (p.nesterov) Vec<GT>::load4(G + off, g[q]);
+          VecNT<float>::load4(M + off, m[q]);
+          VecNT<WT>::load4(W + off, w[q]);
+          if (p.nesterov) VecNT<GT>::load4(G + off, g[q]);
         } else {
           m[q][0] = M[off];
-          w[q][0] = Vec<WT>::load1(W + off);
-          if (p.nesterov) g[q][0] = Vec<GT>::load1(G + off);
+          w[q][0] = VecNT<WT>::load1(W + off);
+          if (p.nesterov) g[q][0] = VecNT<GT>::load1(G + off);
         }
       }
     }
@@ -301,10 +301,10 @@ __global__ __launch_bounds__(256) void rw_tall_apply_kernel(const MatDesc* __res
           w[q][k] = w[q][k] * p.decay - p.lr * dv[k];
         }
         if constexpr (VEC == 4) {
-          Vec<WT>::store4(W + off, w[q]);
-          if (p.write_d) Vec<float>::store4(d.D + off, dv);
+          VecNT<WT>::store4(W + off, w[q]);
+          if (p.write_d) VecNT<float>::store4(d.D + off, dv);
         } else {
-          Vec<WT>::store1(W + off, w[q][0]);
+          VecNT<WT>::store1(W + off, w[q][0]);
           if (p.write_d) d.D[off] = dv[0];
         }
       }
