@@ -160,18 +160,25 @@ constexpr int EPI_LD = BN;                              // fp32 words per staged
 static_assert(QM * EPI_LD * 4 <= STAGE_BYTES, "quarter tile fits a stage buffer");
 
 // byte offset of 16-byte chunk `ch` of tile row `r`: XOR swizzle of the eight
-// 16-byte chunks of a row, so that fragment reads (one row per lane, same chunk)
-// spread over the banks.
-__device__ __forceinline__ int swz(int r, int ch) { return r * ROW_BYTES + ((ch ^ (r & 7)) << 4); }
+// 16-byte chunks of a row by (r / 2) % 8.  A row is 128 B, half of the 64 x 4 B
+// banks, so rows 2a and 2a + 1 share no banks and 16 consecutive rows read at
+// the same chunk (the fragment reads: one row per lane) hit 16 distinct
+// 16-byte bank groups.
+__device__ __forceinline__ int swz_f(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ int swz(int r, int ch) { return r * ROW_BYTES + ((ch ^ swz_f(r)) << 4); }
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(1))) u32x4* gptr4;
 
 // K-major ("TN") stage tile: 64 k-rows of 256 bf16 (512 B, 32 chunks of 16 B);
-// chunk c of row r is stored at c ^ (r % 16).
+// chunk c of row r is stored at c ^ (4 (r % 4)).  A transposing fragment read
+// covers 4 consecutive k-rows x 4 consecutive chunks per 32 lanes; the XOR moves
+// the 4 rows to 4 different 64-byte bank quarters, so those 16 chunks occupy
+// 16 distinct 16-byte bank groups.
 constexpr int TN_ROW_BYTES = BM * 2;
-__device__ __forceinline__ int swz_tn(int r, int ch) { return r * TN_ROW_BYTES + ((ch ^ (r & 15)) << 4); }
+__device__ __forceinline__ int swz_tn_f(int r) { return 4 * (r & 3); }
+__device__ __forceinline__ int swz_tn(int r, int ch) { return r * TN_ROW_BYTES + ((ch ^ swz_tn_f(r)) << 4); }
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16* lds_v4i16;
@@ -183,7 +190,11 @@ typedef __attribute__((address_space(3))) v4i16* lds_v4i16;
 __device__ __forceinline__ int tix(int r, int c) { return r * EPI_LD + (c ^ (((r >> 3) & 7) << 3)); }
 }  // namespace gemm
 
-template <int KIND, DType WD>
+// DIRECT (apply, every iteration but the last): the operands enter the MFMAs
+// swapped, so each lane accumulates four consecutive output columns of one
+// output row, and the bf16 result is stored straight from the accumulators
+// (8 bytes per lane and 32-column block) with no staging through LDS.
+template <int KIND, DType WD, bool DIRECT>
 __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restrict__ md,
                                                          const Item* __restrict__ items,
                                                          NsParams p) {
@@ -219,29 +230,33 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   const int nk = (int)(klen / BK);  // a multiple of 4: the padded dimensions are multiples of the tile
 
   // DMA sources.  NT: wave load q covers tile rows 64 wave + 8 q + lane / 8 and
-  // lane fills physical chunk lane % 8, i.e. logical chunk (lane % 8) ^ (row % 8).
+  // lane fills physical chunk lane % 8, i.e. logical chunk (lane % 8) ^ swz_f(row).
   // TN: wave load q covers k-rows 16 wave + 2 q + lane / 32 and lane fills
-  // physical chunk lane % 32, i.e. logical chunk (lane % 32) ^ (k-row % 16).
+  // physical chunk lane % 32, i.e. logical chunk (lane % 32) ^ swz_tn_f(k-row).
   const uint16_t *srcA, *srcB;
   if constexpr (TN) {
     srcA = P + (int64_t)(16 * wave + (lane >> 5)) * ld + row0;
     srcB = Q + (int64_t)(16 * wave + (lane >> 5)) * ld + col0;
   } else {
-    const int64_t lane_off = (int64_t)(lane >> 3) * ld + (((lane & 7) ^ (lane >> 3)) << 3);
+    // row 64 wave + 8 q + lane / 8: swz_f = 4 (q % 2) + lane / 16, so the
+    // lane's source chunk only depends on the parity of q
+    const int64_t lane_off = (int64_t)(lane >> 3) * ld + (((lane & 7) ^ (lane >> 4)) << 3);
     srcA = P + (row0 + 64 * wave) * ld + lane_off;
     srcB = Q + (col0 + 64 * wave) * ld + lane_off;
   }
   // One 1 KB wave load of the stage at k offset `k`: block q < 8 of operand A,
   // q >= 8 of operand B.
-  auto dma1 = [&](char* stage, int64_t k, int q) {
+  auto dma1 = [&](char* stage, int64_t k, int q) __attribute__((always_inline)) {
     const bool isb = q >= DMA_PER_WAVE;
     const int qq = isb ? q - DMA_PER_WAVE : q;
     const uint16_t* src;
     if constexpr (TN) {
-      const int krow = 2 * qq + (lane >> 5);  // + 16 wave, which is 0 mod 16
-      src = (isb ? srcB : srcA) + (k + 2 * qq) * ld + ((((lane & 31) ^ (krow & 15))) << 3);
+      const int krow = 2 * qq + (lane >> 5);  // + 16 wave, which is 0 mod 4
+      src = (isb ? srcB : srcA) + (k + 2 * qq) * ld + (((lane & 31) ^ swz_tn_f(krow)) << 3);
     } else {
-      src = (isb ? srcB : srcA) + (int64_t)(8 * qq) * ld + k;
+      // chunk bit 2 flips for odd q: (c ^ 4) * 8 elements = c * 8 +- 32
+      const int flip = (qq & 1) ? ((lane & 4) ? -32 : 32) : 0;
+      src = (isb ? srcB : srcA) + (int64_t)(8 * qq) * ld + k + flip;
     }
     __builtin_amdgcn_global_load_lds((const void*)src,
                                      (lds_ptr)(stage + (isb ? A_BYTES : 0) + (DMA_PER_WAVE * wave + qq) * 1024),
@@ -276,19 +291,52 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
       }
   }
 
+  // Apply: the term (a I + diag(dB)) applied to X^T is folded into the
+  // accumulators as one more product, X^T diag(a + dB), taken while the stage
+  // that holds the tile's own columns of X^T passes through LDS.  The diagonal
+  // factor enters the MFMA as a synthetic operand fragment in two bf16 parts
+  // (hi + lo carries 16 mantissa bits; each product is exact in fp32).  Lane L
+  // supplies the diagonal entry of column 32 j + L % 32 at element
+  // e = L % 32 - 16 h - 8 (L / 32) of k-step half h, when 0 <= e < 8.
+  uint32_t fold_hi[NI], fold_lo[NI];
+  if constexpr (KIND == GEMM_APPLY) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const float v = p.a + d.dB[col0 + wn * WN + 32 * j + (lane & 31)];
+      fold_hi[j] = f2bf(v);
+      fold_lo[j] = f2bf(v - bf2f(fold_hi[j]));
+    }
+  }
+  auto syn = [&](uint32_t bits, int h) __attribute__((always_inline)) {
+    const int e = (lane & 31) - 16 * h - 8 * (lane >> 5);
+    const uint32_t word = (e & 1) ? (bits << 16) : bits;
+    u32x4 f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) f[w] = ((unsigned)e < 8u && (e >> 1) == w) ? word : 0u;
+    return __builtin_bit_cast(bf16x8, f);
+  };
+  auto mfma = [&](const bf16x8& x, const bf16x8& y, floatx16& c) __attribute__((always_inline)) {
+    // DIRECT accumulates the transposed block: (P Q^T)^T = Q P^T
+    if constexpr (DIRECT) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y, x, c, 0, 0, 0);
+    else c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, c, 0, 0, 0);
+  };
+
   // Compute one stage from `cur` while streaming stage `knext` (if >= 0) into
   // `nxt`.  The vector-memory path accepts about one 1 KB wave load per 16
   // cycles, so the 16 loads are spread between MFMA sub-groups (4 at the start,
   // then one per 4 MFMAs over the first three k-steps) instead of stalling the
   // in-order issue behind a burst.  Each sub-group also reads 2 of the 8
   // fragments of the next k-step.
-  auto stage_compute = [&](const char* cur, char* nxt, int knext) {
+  // FOLD (apply): 0 none; 1 or 2: the stage is the first or second of the two
+  // stages that hold this wave's output columns as k (block columns 0-1 or 2-3)
+  auto stage_compute = [&](const char* cur, char* nxt, int knext, auto foldc) __attribute__((always_inline)) {
+    constexpr int FOLD = decltype(foldc)::value;
     const char* a = cur;
     const char* b = cur + A_BYTES;
     const int64_t kn = (int64_t)knext * BK;
     const bool more = knext >= 0;
     bf16x8 fa[2][MI], fb[2][NI];
-    auto rd = [&](int set, int i, int ks) {
+    auto rd = [&](int set, int i, int ks) __attribute__((always_inline)) {
       if constexpr (TN) {
         // two transposing reads give lane L the column (L % 32) of the block
         // at 8 consecutive k: k-rows 16 ks + 8 (L / 32) + 4 kk + s, s = 0..3
@@ -311,9 +359,9 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
 #pragma unroll
     for (int i = 0; i < MI; ++i) rd(0, i, 0);
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int cs = ks & 1;
+    auto kstep = [&](auto ksc) __attribute__((always_inline)) {
+      constexpr int ks = decltype(ksc)::value;
+      constexpr int cs = ks & 1;
 #pragma unroll
       for (int i = 0; i < MI; ++i) {          // sub-group: row block i, 4 MFMAs
         if (ks < 3) {
@@ -321,11 +369,27 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
           rd(cs ^ 1, i, ks + 1);
         }
 #pragma unroll
-        for (int j = 0; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cs][i], fb[cs][j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < NI; ++j) mfma(fa[cs][i], fb[cs][j], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
-    }
+      if constexpr (FOLD != 0) {
+        constexpr int J = 2 * (FOLD - 1) + ks / 2;
+        // opaque here, so the fragments are built in the fold stage and not
+        // hoisted out of the main loop (they would hold 64 registers)
+        uint32_t hb = fold_hi[J], lb = fold_lo[J];
+        asm volatile("" : "+v"(hb), "+v"(lb));
+        const bf16x8 hi = syn(hb, ks & 1), lo = syn(lb, ks & 1);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) mfma(fa[cs][i], hi, acc[i][J]);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) mfma(fa[cs][i], lo, acc[i][J]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    kstep(std::integral_constant<int, 0>{});
+    kstep(std::integral_constant<int, 1>{});
+    kstep(std::integral_constant<int, 2>{});
+    kstep(std::integral_constant<int, 3>{});
   };
   static_assert(NDMA == 16 && BK / 16 == 4 && MI == 4, "schedule assumes 16 loads, 4 k-steps, 4 row blocks");
 
@@ -333,17 +397,62 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
 #pragma unroll
   for (int q = 0; q < NDMA; ++q) dma1(s0, 0, q);
   __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    stage_compute(s0, s1, kt + 1);
+  auto stage_pair = [&](int kt, auto f0, auto f1) __attribute__((always_inline)) {
+    stage_compute(s0, s1, kt + 1, f0);
     __syncthreads();  // stage kt+1 has landed; every wave is done with s0
-    stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1);
+    stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1, f1);
     __syncthreads();
+  };
+  constexpr std::integral_constant<int, 0> nofold{};
+  // apply: the stage pair that carries this wave's output columns as k runs
+  // between two plain loops (one loop body with both variants spills)
+  const int kfold = (KIND == GEMM_APPLY) ? (int)((col0 + wn * WN) / BK) : nk;
+  int kt = 0;
+  for (; kt < kfold; kt += 2) stage_pair(kt, nofold, nofold);
+  if constexpr (KIND == GEMM_APPLY) {
+    stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{});
+    kt += 2;
+    for (; kt < nk; kt += 2) stage_pair(kt, nofold, nofold);
   }
 
   const bool sym = (KIND != GEMM_APPLY);
   const bool diag = sym && it.tm == it.tn;
   const bool last = (KIND == GEMM_APPLY) && p.last;
   const float alpha = (p.iter == 0) ? *d.alpha : 1.0f;
+  if constexpr (DIRECT) {
+    // The whole 256 x 256 tile is staged once in LDS as bf16 (rows 0..127 in
+    // s0, 128..255 in s1; 512 B per row, 16-byte chunk c of row r stored at
+    // c ^ (r % 32)), then written out in full 512-byte row segments.
+    // Lane L holds output row 32 i + L % 32 of its wave block and, for block
+    // column j and q = 0..3, the 4 columns 32 j + 8 q + 4 (L / 32) + 0..3.
+    char* T = wm ? s1 : s0;
+    const int hl = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int r = 32 * i + (lane & 31);
+      char* trow = T + r * 512 + 8 * hl;
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int ch = (wn * WN + 32 * j + 8 * q) >> 3;
+          uint2 w;
+          w.x = pack_bf2(alpha * acc[i][j][4 * q + 0], alpha * acc[i][j][4 * q + 1]);
+          w.y = pack_bf2(alpha * acc[i][j][4 * q + 2], alpha * acc[i][j][4 * q + 3]);
+          *reinterpret_cast<uint2*>(trow + ((ch ^ (r & 31)) << 4)) = w;
+        }
+    }
+    __syncthreads();
+    const int ch = tid & 31;
+#pragma unroll 4
+    for (int it = 0; it < BM / 8; ++it) {
+      const int row = it * 8 + (tid >> 5);
+      const char* src = (row < 128 ? s0 : s1) + (row & 127) * 512 + ((ch ^ (row & 31)) << 4);
+      const u32x4 w = *reinterpret_cast<const u32x4*>(src);
+      *reinterpret_cast<u32x4*>(XTo + (row0 + row) * rp + col0 + ch * 8) = w;
+    }
+    return;
+  }
   // transposed outputs: Gram/square mirror tiles, and the parameter write of a
   // wide matrix (the apply tile is a tile of X^T)
   const bool need_t = (sym && !diag) || (last && !d.tall);
@@ -356,7 +465,7 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   const int ec = (tid % TPRW) * EPR, er = tid / TPRW;
   // Accumulator rows of MFMA blocks IB, IB+1 (one quarter) into the staging tile.
   // acc[] needs static indices, so the block offset is a template parameter.
-  auto stage_acc = [&](float* T, auto ibc) {
+  auto stage_acc = [&](float* T, auto ibc) __attribute__((always_inline)) {
     constexpr int IB = decltype(ibc)::value;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -379,15 +488,14 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
       else stage_acc(T, std::integral_constant<int, 0>{});
     }
     const int64_t qrow0 = row0 + h * QM;
-    // inputs of the natural-layout pass (XT for apply, Ao for the square)
+    // input of the natural-layout pass of the square: Ao
     u32x4 xin[NPASS];  // packed bf16
-    if constexpr (KIND != GEMM_GRAM) {
-      const uint16_t* src = (KIND == GEMM_APPLY) ? XTc : d.Ao;
+    if constexpr (KIND == GEMM_POLY) {
 #pragma unroll
       for (int ps = 0; ps < NPASS; ++ps)
-        xin[ps] = *(gptr4)(src + (qrow0 + ps * RPP + er) * rp + col0 + ec);
+        xin[ps] = *(gptr4)(d.Ao + (qrow0 + ps * RPP + er) * rp + col0 + ec);
     }
-    auto xval = [&](int ps, int q) {
+    auto xval = [&](int ps, int q) __attribute__((always_inline)) {
       const uint32_t w = xin[ps][q >> 1];
       return bf2f((q & 1) ? (w >> 16) : (w & 0xffffu));
     };
@@ -428,11 +536,9 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
         }
         Vec<uint16_t>::store8(d.Bo + gi * rp + gj, v);
       } else {
-        // X'^T[gi][gj] = alpha ((a + dB[gj]) XT[gi][gj] + (XT Bo)[gi][gj])
-        float db[EPR];
-        Vec<float>::load8(d.dB + gj, db);
+        // X'^T = alpha (XT diag(a + dB) + XT Bo); the first term is in acc
 #pragma unroll
-        for (int q = 0; q < EPR; ++q) v[q] = alpha * ((p.a + db[q]) * xval(ps, q) + v[q]);
+        for (int q = 0; q < EPR; ++q) v[q] = alpha * v[q];
         if (!last) {
           Vec<uint16_t>::store8(XTo + gi * rp + gj, v);
         } else if (d.tall) {
@@ -545,11 +651,12 @@ hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item
   if (nitems <= 0) return hipSuccess;
   dim3 g(nitems), b(gemm::NTHREADS);
   switch (kind) {
-    case GEMM_GRAM: ns_gemm_kernel<GEMM_GRAM, BF16><<<g, b, 0, s>>>(md, items, p); break;
-    case GEMM_POLY: ns_gemm_kernel<GEMM_POLY, BF16><<<g, b, 0, s>>>(md, items, p); break;
+    case GEMM_GRAM: ns_gemm_kernel<GEMM_GRAM, BF16, false><<<g, b, 0, s>>>(md, items, p); break;
+    case GEMM_POLY: ns_gemm_kernel<GEMM_POLY, BF16, false><<<g, b, 0, s>>>(md, items, p); break;
     case GEMM_APPLY:
-      if (wt == BF16) ns_gemm_kernel<GEMM_APPLY, BF16><<<g, b, 0, s>>>(md, items, p);
-      else ns_gemm_kernel<GEMM_APPLY, F32><<<g, b, 0, s>>>(md, items, p);
+      if (!p.last) ns_gemm_kernel<GEMM_APPLY, BF16, true><<<g, b, 0, s>>>(md, items, p);
+      else if (wt == BF16) ns_gemm_kernel<GEMM_APPLY, BF16, false><<<g, b, 0, s>>>(md, items, p);
+      else ns_gemm_kernel<GEMM_APPLY, F32, false><<<g, b, 0, s>>>(md, items, p);
       break;
     default: return hipErrorInvalidValue;
   }
