@@ -148,13 +148,24 @@ __global__ __launch_bounds__(256) void ns_alpha_kernel(const MatDesc* __restrict
 // ---------------------------------------------------------------------------
 namespace gemm {
 constexpr int BM = kNsTile, BN = kNsTile, BK = 64;
-constexpr int NTHREADS = 256;
-constexpr int WM = BM / 2, WN = BN / 2;  // 2 x 2 waves
+#ifndef PRM_GEMM_WAVES_N
+#define PRM_GEMM_WAVES_N 2
+#endif
+// waves: 2 along the tile rows x WAVES_N along the columns.  2 x 2 (one wave
+// per SIMD, 128 x 128 per wave) is the default; 2 x 4 (two waves per SIMD,
+// 128 x 64 each) reads 1.5x more fragment bytes from LDS per MFMA and measured
+// about 2% slower over the DiT-4B weight set.
+constexpr int WAVES_M = 2, WAVES_N = PRM_GEMM_WAVES_N, NWAVES = WAVES_M * WAVES_N;
+constexpr int NTHREADS = 64 * NWAVES;
+constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
 constexpr int MI = WM / 32, NI = WN / 32;
 constexpr int ROW_BYTES = BK * 2;                       // 128 B per tile row
 constexpr int A_BYTES = BM * ROW_BYTES;                 // 32 KB
 constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;      // 64 KB
-constexpr int DMA_PER_WAVE = BM / 8 / 4;                // 1 KB wave loads per operand per stage
+constexpr int DMA_PER_WAVE = BM / 8 / NWAVES;           // 1 KB wave loads per operand per stage
+constexpr int NDMA = 2 * DMA_PER_WAVE;                  // wave loads per stage (both operands)
+constexpr int ROWS_PER_WAVE = BM / NWAVES;              // NT: tile rows one wave loads per operand
+constexpr int KROWS_PER_WAVE = BK / NWAVES;             // TN: k-rows one wave loads per operand
 constexpr int QM = 64;                                  // epilogue quarter rows
 constexpr int EPI_LD = BN;                              // fp32 words per staged row
 static_assert(QM * EPI_LD * 4 <= STAGE_BYTES, "quarter tile fits a stage buffer");
@@ -195,7 +206,7 @@ __device__ __forceinline__ int tix(int r, int c) { return r * EPI_LD + (c ^ (((r
 // output row, and the bf16 result is stored straight from the accumulators
 // (8 bytes per lane and 32-column block) with no staging through LDS.
 template <int KIND, DType WD, bool DIRECT>
-__global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restrict__ md,
+__global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDesc* __restrict__ md,
                                                          const Item* __restrict__ items,
                                                          NsParams p) {
   using namespace gemm;
@@ -207,7 +218,7 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   const MatDesc& d = md[it.mat];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const bool even = (p.iter & 1) == 0;
   const uint16_t* XTc = even ? d.XT : d.XTn;
   uint16_t* XTo = even ? d.XTn : d.XT;
@@ -229,29 +240,31 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   const int64_t row0 = (int64_t)it.tm * BM, col0 = (int64_t)it.tn * BN;
   const int nk = (int)(klen / BK);  // a multiple of 4: the padded dimensions are multiples of the tile
 
-  // DMA sources.  NT: wave load q covers tile rows 64 wave + 8 q + lane / 8 and
-  // lane fills physical chunk lane % 8, i.e. logical chunk (lane % 8) ^ swz_f(row).
-  // TN: wave load q covers k-rows 16 wave + 2 q + lane / 32 and lane fills
-  // physical chunk lane % 32, i.e. logical chunk (lane % 32) ^ swz_tn_f(k-row).
+  // DMA sources.  NT: wave load q covers tile rows R wave + 8 q + lane / 8
+  // (R = ROWS_PER_WAVE, a multiple of 16) and lane fills physical chunk lane % 8,
+  // i.e. logical chunk (lane % 8) ^ swz_f(row).  TN: wave load q covers k-rows
+  // KR wave + 2 q + lane / 32 (KR = KROWS_PER_WAVE, a multiple of 4) and lane
+  // fills physical chunk lane % 32, i.e. logical chunk (lane % 32) ^ swz_tn_f(k-row).
+  static_assert(ROWS_PER_WAVE % 16 == 0 && KROWS_PER_WAVE % 4 == 0, "swizzle phase per wave");
   const uint16_t *srcA, *srcB;
   if constexpr (TN) {
-    srcA = P + (int64_t)(16 * wave + (lane >> 5)) * ld + row0;
-    srcB = Q + (int64_t)(16 * wave + (lane >> 5)) * ld + col0;
+    srcA = P + (int64_t)(KROWS_PER_WAVE * wave + (lane >> 5)) * ld + row0;
+    srcB = Q + (int64_t)(KROWS_PER_WAVE * wave + (lane >> 5)) * ld + col0;
   } else {
-    // row 64 wave + 8 q + lane / 8: swz_f = 4 (q % 2) + lane / 16, so the
-    // lane's source chunk only depends on the parity of q
+    // swz_f(row) = 4 (q % 2) + lane / 16, so the lane's source chunk only
+    // depends on the parity of q
     const int64_t lane_off = (int64_t)(lane >> 3) * ld + (((lane & 7) ^ (lane >> 4)) << 3);
-    srcA = P + (row0 + 64 * wave) * ld + lane_off;
-    srcB = Q + (col0 + 64 * wave) * ld + lane_off;
+    srcA = P + (row0 + ROWS_PER_WAVE * wave) * ld + lane_off;
+    srcB = Q + (col0 + ROWS_PER_WAVE * wave) * ld + lane_off;
   }
-  // One 1 KB wave load of the stage at k offset `k`: block q < 8 of operand A,
-  // q >= 8 of operand B.
+  // One 1 KB wave load of the stage at k offset `k`: block q < DMA_PER_WAVE of
+  // operand A, the others of operand B.
   auto dma1 = [&](char* stage, int64_t k, int q) __attribute__((always_inline)) {
     const bool isb = q >= DMA_PER_WAVE;
     const int qq = isb ? q - DMA_PER_WAVE : q;
     const uint16_t* src;
     if constexpr (TN) {
-      const int krow = 2 * qq + (lane >> 5);  // + 16 wave, which is 0 mod 4
+      const int krow = 2 * qq + (lane >> 5);  // + KR wave, which is 0 mod 4
       src = (isb ? srcB : srcA) + (k + 2 * qq) * ld + (((lane & 31) ^ swz_tn_f(krow)) << 3);
     } else {
       // chunk bit 2 flips for odd q: (c ^ 4) * 8 elements = c * 8 +- 32
@@ -262,7 +275,6 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
                                      (lds_ptr)(stage + (isb ? A_BYTES : 0) + (DMA_PER_WAVE * wave + qq) * 1024),
                                      16, 0, 0);
   };
-  constexpr int NDMA = 2 * DMA_PER_WAVE;  // 16 wave loads per stage
 
   floatx16 acc[MI][NI];
 #pragma unroll
@@ -276,19 +288,23 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   const int khalf = lane >> 5;
   // TN fragment addresses (k-step 0): lane L of 16-lane group g = L / 16 reads
   // k-row 8 (g / 2) + 4 kk + (L % 16) / 4 at columns m0 + 16 (g % 2) + 4 (L % 4)
-  int tn_off[MI][2], tn_offb[MI][2];
+  int tn_off[MI][2], tn_offb[NI][2];
   if constexpr (TN) {
     const int g = lane >> 4, jl = lane & 15;
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
+    for (int kk = 0; kk < 2; ++kk) {
+      const int kr = 8 * (g >> 1) + 4 * kk + (jl >> 2);
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const int kr = 8 * (g >> 1) + 4 * kk + (jl >> 2);
+      for (int i = 0; i < MI; ++i) {
         const int ma = wm * WM + i * 32 + 16 * (g & 1) + 4 * (jl & 3);
-        const int mb = wn * WN + i * 32 + 16 * (g & 1) + 4 * (jl & 3);
         tn_off[i][kk] = swz_tn(kr, ma >> 3) + ((ma & 7) << 1);
-        tn_offb[i][kk] = swz_tn(kr, mb >> 3) + ((mb & 7) << 1);
       }
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int mb = wn * WN + j * 32 + 16 * (g & 1) + 4 * (jl & 3);
+        tn_offb[j][kk] = swz_tn(kr, mb >> 3) + ((mb & 7) << 1);
+      }
+    }
   }
 
   // Apply: the term (a I + diag(dB)) applied to X^T is folded into the
@@ -323,57 +339,64 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
 
   // Compute one stage from `cur` while streaming stage `knext` (if >= 0) into
   // `nxt`.  The vector-memory path accepts about one 1 KB wave load per 16
-  // cycles, so the 16 loads are spread between MFMA sub-groups (4 at the start,
-  // then one per 4 MFMAs over the first three k-steps) instead of stalling the
-  // in-order issue behind a burst.  Each sub-group also reads 2 of the 8
-  // fragments of the next k-step.
-  // FOLD (apply): 0 none; 1 or 2: the stage is the first or second of the two
-  // stages that hold this wave's output columns as k (block columns 0-1 or 2-3)
-  auto stage_compute = [&](const char* cur, char* nxt, int knext, auto foldc) __attribute__((always_inline)) {
+  // cycles, so the wave's loads are spread between MFMA sub-groups (a quarter
+  // at the start, the rest over the first three k-steps) instead of stalling
+  // the in-order issue behind a burst.  Sub-group i (row block i) also reads the
+  // next k-step's A fragment i and, for i < NI, its B fragment i.
+  // FOLD (apply): 0 none; f >= 1: the stage holds this wave's output block
+  // columns 2 (f - 1) and 2 (f - 1) + 1 as k
+  // (one stage per wave, WN == BK): `fold` selects it at run time instead
+  auto stage_compute = [&](const char* cur, char* nxt, int knext, auto foldc, bool fold) __attribute__((always_inline)) {
     constexpr int FOLD = decltype(foldc)::value;
     const char* a = cur;
     const char* b = cur + A_BYTES;
     const int64_t kn = (int64_t)knext * BK;
     const bool more = knext >= 0;
     bf16x8 fa[2][MI], fb[2][NI];
-    auto rd = [&](int set, int i, int ks) __attribute__((always_inline)) {
-      if constexpr (TN) {
-        // two transposing reads give lane L the column (L % 32) of the block
-        // at 8 consecutive k: k-rows 16 ks + 8 (L / 32) + 4 kk + s, s = 0..3
-        v4i16 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(a + tn_off[i][0] + ks * 16 * TN_ROW_BYTES));
-        v4i16 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(a + tn_off[i][1] + ks * 16 * TN_ROW_BYTES));
-        v4i16 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(b + tn_offb[i][0] + ks * 16 * TN_ROW_BYTES));
-        v4i16 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(b + tn_offb[i][1] + ks * 16 * TN_ROW_BYTES));
-        fa[set][i] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
-        fb[set][i] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7));
-      } else {
-        const int ch = ks * 2 + khalf;
-        fa[set][i] = *reinterpret_cast<const bf16x8*>(a + swz(arow + i * 32, ch));
-        fb[set][i] = *reinterpret_cast<const bf16x8*>(b + swz(brow + i * 32, ch));
-      }
+    // two transposing reads give lane L the column (L % 32) of the block at 8
+    // consecutive k: k-rows 16 ks + 8 (L / 32) + 4 kk + s, s = 0..3
+    auto rd_tn = [&](const char* base, const int (&off)[2], int ks) __attribute__((always_inline)) {
+      v4i16 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(base + off[0] + ks * 16 * TN_ROW_BYTES));
+      v4i16 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(base + off[1] + ks * 16 * TN_ROW_BYTES));
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7));
     };
+    auto rda = [&](int set, int i, int ks) __attribute__((always_inline)) {
+      if constexpr (TN) fa[set][i] = rd_tn(a, tn_off[i], ks);
+      else fa[set][i] = *reinterpret_cast<const bf16x8*>(a + swz(arow + i * 32, ks * 2 + khalf));
+    };
+    auto rdb = [&](int set, int j, int ks) __attribute__((always_inline)) {
+      if constexpr (TN) fb[set][j] = rd_tn(b, tn_offb[j], ks);
+      else fb[set][j] = *reinterpret_cast<const bf16x8*>(b + swz(brow + j * 32, ks * 2 + khalf));
+    };
+    // loads at the start; the rest go one per DMA_SLOT-th sub-group over k-steps 0..2
+    constexpr int DMA0 = NDMA / 4, DMA_SLOT = (3 * MI) / (NDMA - DMA0);
+    static_assert((NDMA - DMA0) * DMA_SLOT == 3 * MI, "loads spread evenly over three k-steps");
     if (more) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) dma1(nxt, kn, q);
+      for (int q = 0; q < DMA0; ++q) dma1(nxt, kn, q);
     }
 #pragma unroll
-    for (int i = 0; i < MI; ++i) rd(0, i, 0);
+    for (int i = 0; i < MI; ++i) rda(0, i, 0);
+#pragma unroll
+    for (int j = 0; j < NI; ++j) rdb(0, j, 0);
     __builtin_amdgcn_sched_barrier(0);
     auto kstep = [&](auto ksc) __attribute__((always_inline)) {
       constexpr int ks = decltype(ksc)::value;
       constexpr int cs = ks & 1;
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {          // sub-group: row block i, 4 MFMAs
+      for (int i = 0; i < MI; ++i) {          // sub-group: row block i, NI MFMAs
         if (ks < 3) {
-          if (more) dma1(nxt, kn, 4 + ks * 4 + i);
-          rd(cs ^ 1, i, ks + 1);
+          const int slot = ks * MI + i;
+          if (more && slot % DMA_SLOT == 0) dma1(nxt, kn, DMA0 + slot / DMA_SLOT);
+          rda(cs ^ 1, i, ks + 1);
+          if (i < NI) rdb(cs ^ 1, i, ks + 1);
         }
 #pragma unroll
         for (int j = 0; j < NI; ++j) mfma(fa[cs][i], fb[cs][j], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
-      if constexpr (FOLD != 0) {
-        constexpr int J = 2 * (FOLD - 1) + ks / 2;
+      if (FOLD != 0 && fold) {
+        constexpr int J = (FOLD > 0 ? 2 * (FOLD - 1) : 0) + ks / 2;
         // opaque here, so the fragments are built in the fold stage and not
         // hoisted out of the main loop (they would hold 64 registers)
         uint32_t hb = fold_hi[J], lb = fold_lo[J];
@@ -391,28 +414,36 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
     kstep(std::integral_constant<int, 2>{});
     kstep(std::integral_constant<int, 3>{});
   };
-  static_assert(NDMA == 16 && BK / 16 == 4 && MI == 4, "schedule assumes 16 loads, 4 k-steps, 4 row blocks");
+  static_assert(BK / 16 == 4 && MI == 4 && NI <= MI, "schedule assumes 4 k-steps, 4 row blocks");
 
   // stage 0 up front, then ping-pong: s0 holds even stages, s1 odd ones
 #pragma unroll
   for (int q = 0; q < NDMA; ++q) dma1(s0, 0, q);
   __syncthreads();
-  auto stage_pair = [&](int kt, auto f0, auto f1) __attribute__((always_inline)) {
-    stage_compute(s0, s1, kt + 1, f0);
+  auto stage_pair = [&](int kt, auto f0, auto f1, bool fold0, bool fold1) __attribute__((always_inline)) {
+    stage_compute(s0, s1, kt + 1, f0, fold0);
     __syncthreads();  // stage kt+1 has landed; every wave is done with s0
-    stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1, f1);
+    stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1, f1, fold1);
     __syncthreads();
   };
   constexpr std::integral_constant<int, 0> nofold{};
-  // apply: the stage pair that carries this wave's output columns as k runs
-  // between two plain loops (one loop body with both variants spills)
+  // apply: the stage(s) that carry this wave's output columns as k
   const int kfold = (KIND == GEMM_APPLY) ? (int)((col0 + wn * WN) / BK) : nk;
   int kt = 0;
-  for (; kt < kfold; kt += 2) stage_pair(kt, nofold, nofold);
-  if constexpr (KIND == GEMM_APPLY) {
-    stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{});
-    kt += 2;
-    for (; kt < nk; kt += 2) stage_pair(kt, nofold, nofold);
+  if constexpr (KIND == GEMM_APPLY && WN == BK) {
+    // one stage: a run-time flag in a single loop (J is static either way)
+    constexpr std::integral_constant<int, -1> fold_rt{};
+    for (; kt < nk; kt += 2) stage_pair(kt, fold_rt, fold_rt, kt == kfold, kt + 1 == kfold);
+  } else {
+    // two stages (a stage pair): it runs between two plain loops, since one
+    // loop body holding both variants spills
+    for (; kt < (kfold & ~1); kt += 2) stage_pair(kt, nofold, nofold, false, false);
+    if constexpr (KIND == GEMM_APPLY) {
+      static_assert(WN == 2 * BK, "a wave's output columns span one or two stages");
+      stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, true, true);
+      kt += 2;
+      for (; kt < nk; kt += 2) stage_pair(kt, nofold, nofold, false, false);
+    }
   }
 
   const bool sym = (KIND != GEMM_APPLY);
@@ -444,9 +475,10 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
     }
     __syncthreads();
     const int ch = tid & 31;
+    constexpr int ROWS_PER_IT = NTHREADS / 32;
 #pragma unroll 4
-    for (int it = 0; it < BM / 8; ++it) {
-      const int row = it * 8 + (tid >> 5);
+    for (int it = 0; it < BM / ROWS_PER_IT; ++it) {
+      const int row = it * ROWS_PER_IT + (tid >> 5);
       const char* src = (row < 128 ? s0 : s1) + (row & 127) * 512 + ((ch ^ (row & 31)) << 4);
       const u32x4 w = *reinterpret_cast<const u32x4*>(src);
       *reinterpret_cast<u32x4*>(XTo + (row0 + row) * rp + col0 + ch * 8) = w;
@@ -460,8 +492,8 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(const MatDesc* __restri
   // Epilogue in four quarters of QM rows, staged alternately in s0 and s1.
   constexpr int EPR = 8;                    // consecutive elements per thread
   constexpr int TPRW = BN / EPR;            // threads per staged row (32)
-  constexpr int RPP = NTHREADS / TPRW;      // rows per pass (8)
-  constexpr int NPASS = QM / RPP;           // 8
+  constexpr int RPP = NTHREADS / TPRW;      // rows per pass
+  constexpr int NPASS = QM / RPP;
   const int ec = (tid % TPRW) * EPR, er = tid / TPRW;
   // Accumulator rows of MFMA blocks IB, IB+1 (one quarter) into the staging tile.
   // acc[] needs static indices, so the block offset is a template parameter.
