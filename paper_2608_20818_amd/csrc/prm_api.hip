@@ -301,8 +301,16 @@ void build_lists(Plan& P, const prm_config* cfg) {
     for (size_t k = 0; k < ch.mats.size(); ++k) {
       const int i = ch.mats[k];
       const int32_t tr = (int32_t)(P.rp[i] / kNsTile), tc = (int32_t)(P.cp[i] / kNsTile);
+      // Gram and square: each matrix's (upper) tiles stay on one XCD, whose 32
+      // CUs then share its r x r panels in their L2
       tile_order(i, tr, tr, true, g[k % kXcds]);
-      tile_order(i, tc, tr, false, a[k % kXcds]);  // tiles of X'^T: rows over c, columns over r
+      // apply: every XCD takes a contiguous eighth of each matrix's tile order,
+      // so all XCDs stream the same Bo at the same time (it is read by every
+      // tile row; the last-level cache then serves the repeats)
+      std::vector<Item> ta;
+      tile_order(i, tc, tr, false, ta);  // tiles of X'^T: rows over c, columns over r
+      for (int x = 0; x < kXcds; ++x)
+        a[x].insert(a[x].end(), ta.begin() + ta.size() * x / kXcds, ta.begin() + ta.size() * (x + 1) / kXcds);
     }
     ch.gram = interleave_xcd(g);
     ch.poly = ch.gram;
