@@ -332,8 +332,8 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     return __builtin_bit_cast(bf16x8, f);
   };
   auto mfma = [&](const bf16x8& x, const bf16x8& y, floatx16& c) __attribute__((always_inline)) {
-    // DIRECT accumulates the transposed block: (P Q^T)^T = Q P^T
-    if constexpr (DIRECT) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y, x, c, 0, 0, 0);
+    // DIRECT and the Gram accumulate the transposed block: (P Q^T)^T = Q P^T
+    if constexpr (DIRECT || KIND == GEMM_GRAM) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y, x, c, 0, 0, 0);
     else c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, c, 0, 0, 0);
   };
 
@@ -485,7 +485,80 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     }
     return;
   }
-  // transposed outputs: Gram/square mirror tiles, and the parameter write of a
+  if constexpr (KIND == GEMM_GRAM) {
+    // A = alpha^2 acc: the diagonal goes to dA (fp32), the rest to Ao (bf16).
+    // The tile is staged once in LDS as bf16 (layout as for DIRECT), written
+    // as 512-byte row segments, and for a tile above the diagonal also as its
+    // mirror: transposing reads (ds_read_b64_tr_b16) give each lane 8
+    // consecutive tile rows of one tile column, i.e. 16 bytes of a row of the
+    // mirrored tile.
+    const float s2 = alpha * alpha;
+    char* T = wm ? s1 : s0;
+    const int hl = lane >> 5, m = lane & 31;
+    // lane L holds A[r][r] of a diagonal block iff (L % 32) / 4 % 2 == L / 32,
+    // at q = (L % 32) / 8, element (L % 32) % 4
+    const bool dlane = diag && wm == wn && ((m >> 2) & 1) == hl;
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int r = 32 * i + m;
+      char* trow = T + r * 512 + 8 * hl;
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = s2 * acc[i][j][4 * q + e];
+          if (i == j && dlane && q == (m >> 3)) {
+            float dv = v[0];
+#pragma unroll
+            for (int e = 1; e < 4; ++e) dv = (e == (m & 3)) ? v[e] : dv;
+            d.dA[row0 + wm * WM + r] = dv;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = (e == (m & 3)) ? 0.f : v[e];
+          }
+          const int ch = (wn * WN + 32 * j + 8 * q) >> 3;
+          uint2 w;
+          w.x = pack_bf2(v[0], v[1]);
+          w.y = pack_bf2(v[2], v[3]);
+          *reinterpret_cast<uint2*>(trow + ((ch ^ (r & 31)) << 4)) = w;
+        }
+    }
+    __syncthreads();
+    auto tbyte = [&](int row, int col) __attribute__((always_inline)) {
+      return (row < 128 ? s0 : s1) + (row & 127) * 512 + ((((col >> 3) ^ (row & 31))) << 4) + (col & 7) * 2;
+    };
+    const int ch = tid & 31;
+    constexpr int ROWS_PER_IT = NTHREADS / 32;
+#pragma unroll 4
+    for (int itr = 0; itr < BM / ROWS_PER_IT; ++itr) {
+      const int row = itr * ROWS_PER_IT + (tid >> 5);
+      const u32x4 w = *reinterpret_cast<const u32x4*>(tbyte(row, ch * 8));
+      *reinterpret_cast<u32x4*>(d.Ao + (row0 + row) * rp + col0 + ch * 8) = w;
+    }
+    if (!diag) {
+      // 16-lane group g reads tile rows R0 .. R0 + 7 (R0 = 32 rb + 8 g) of
+      // columns C0 .. C0 + 15; source lane 4 a + b of the group points at
+      // row R0 + a (+4), columns C0 + 4 b .. +3
+      const int g = lane >> 4, li = lane & 15;
+      constexpr int CB = BN / 16 / NWAVES;  // 16-column blocks per wave
+#pragma unroll 2
+      for (int cb = 0; cb < CB; ++cb) {
+        const int C0 = (wave * CB + cb) * 16;
+#pragma unroll 4
+        for (int rb = 0; rb < BM / 32; ++rb) {
+          const int R0 = 32 * rb + 8 * g;
+          const int sr = R0 + (li >> 2), sc = C0 + 4 * (li & 3);
+          const v4i16 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr, sc));
+          const v4i16 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr + 4, sc));
+          const u32x4 w = __builtin_bit_cast(u32x4, __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7));
+          *reinterpret_cast<u32x4*>(d.Ao + (col0 + C0 + li) * rp + row0 + R0) = w;
+        }
+      }
+    }
+    return;
+  }
+  // transposed outputs: square mirror tiles, and the parameter write of a
   // wide matrix (the apply tile is a tile of X^T)
   const bool need_t = (sym && !diag) || (last && !d.tall);
 
