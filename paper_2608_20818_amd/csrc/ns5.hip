@@ -332,8 +332,9 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     return __builtin_bit_cast(bf16x8, f);
   };
   auto mfma = [&](const bf16x8& x, const bf16x8& y, floatx16& c) __attribute__((always_inline)) {
-    // DIRECT and the Gram accumulate the transposed block: (P Q^T)^T = Q P^T
-    if constexpr (DIRECT || KIND == GEMM_GRAM) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y, x, c, 0, 0, 0);
+    // DIRECT, the Gram and the square accumulate the transposed block:
+    // (P Q^T)^T = Q P^T
+    if constexpr (DIRECT || KIND != GEMM_APPLY) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y, x, c, 0, 0, 0);
     else c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, c, 0, 0, 0);
   };
 
@@ -485,44 +486,86 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     }
     return;
   }
-  if constexpr (KIND == GEMM_GRAM) {
-    // A = alpha^2 acc: the diagonal goes to dA (fp32), the rest to Ao (bf16).
-    // The tile is staged once in LDS as bf16 (layout as for DIRECT), written
-    // as 512-byte row segments, and for a tile above the diagonal also as its
+  if constexpr (KIND != GEMM_APPLY) {
+    // Gram: A = alpha^2 acc; the diagonal goes to dA (fp32), the rest to Ao.
+    // Square: A^2 = dA^2 + dA Ao + Ao dA + Ao Ao with acc = Ao Ao, and
+    // B = b A + c A^2; the diagonal goes to dB (fp32), the rest to Bo.
+    // The tile is staged once in LDS as bf16 (layout as for DIRECT), written as
+    // 512-byte row segments, and for a tile above the diagonal also as its
     // mirror: transposing reads (ds_read_b64_tr_b16) give each lane 8
     // consecutive tile rows of one tile column, i.e. 16 bytes of a row of the
     // mirrored tile.
+    uint16_t* out = (KIND == GEMM_GRAM) ? d.Ao : d.Bo;
+    float* dout = (KIND == GEMM_GRAM) ? d.dA : d.dB;
     const float s2 = alpha * alpha;
     char* T = wm ? s1 : s0;
     const int hl = lane >> 5, m = lane & 31;
-    // lane L holds A[r][r] of a diagonal block iff (L % 32) / 4 % 2 == L / 32,
-    // at q = (L % 32) / 8, element (L % 32) % 4
+    // lane L holds the (r, r) entry of a diagonal block iff (L % 32) / 4 % 2
+    // == L / 32, at q = (L % 32) / 8, element (L % 32) % 4
     const bool dlane = diag && wm == wn && ((m >> 2) & 1) == hl;
-#pragma unroll
-    for (int i = 0; i < MI; ++i) {
-      const int r = 32 * i + m;
-      char* trow = T + r * 512 + 8 * hl;
+    const int64_t grow = row0 + wm * WM + m, gcol = col0 + wn * WN + 4 * hl;
+    // square: dA of this lane's columns (the same for every row block)
+    float dcol[NI][4][4];
+    if constexpr (KIND == GEMM_POLY) {
 #pragma unroll
       for (int j = 0; j < NI; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float v[4];
+        for (int q = 0; q < 4; ++q) Vec<float>::load4(d.dA + gcol + 32 * j + 8 * q, dcol[j][q]);
+    }
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = s2 * acc[i][j][4 * q + e];
-          if (i == j && dlane && q == (m >> 3)) {
-            float dv = v[0];
+    for (int ih = 0; ih < MI; ih += 2) {
+      // square: Ao and dA of rows 32 i + L % 32 for two row blocks
+      uint2 ao[2][NI][4];
+      float drow[2];
+      if constexpr (KIND == GEMM_POLY) {
 #pragma unroll
-            for (int e = 1; e < 4; ++e) dv = (e == (m & 3)) ? v[e] : dv;
-            d.dA[row0 + wm * WM + r] = dv;
+        for (int ii = 0; ii < 2; ++ii) {
+          const int64_t gr = grow + 32 * (ih + ii);
+          drow[ii] = d.dA[gr];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = (e == (m & 3)) ? 0.f : v[e];
-          }
-          const int ch = (wn * WN + 32 * j + 8 * q) >> 3;
-          uint2 w;
-          w.x = pack_bf2(v[0], v[1]);
-          w.y = pack_bf2(v[2], v[3]);
-          *reinterpret_cast<uint2*>(trow + ((ch ^ (r & 31)) << 4)) = w;
+          for (int j = 0; j < NI; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              ao[ii][j][q] = *reinterpret_cast<const uint2*>(d.Ao + gr * rp + gcol + 32 * j + 8 * q);
         }
+      }
+#pragma unroll
+      for (int ii = 0; ii < 2; ++ii) {
+        const int i = ih + ii;
+        const int r = 32 * i + m;
+        char* trow = T + r * 512 + 8 * hl;
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float v[4];
+            if constexpr (KIND == GEMM_GRAM) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = s2 * acc[i][j][4 * q + e];
+            } else {
+              const uint2 w2 = ao[ii][j][q];
+              const float a4[4] = {bf2f(w2.x & 0xffffu), bf2f(w2.x >> 16), bf2f(w2.y & 0xffffu), bf2f(w2.y >> 16)};
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                v[e] = p.c * acc[i][j][4 * q + e] + (p.b + p.c * (drow[ii] + dcol[j][q][e])) * a4[e];
+            }
+            if (i == j && dlane && q == (m >> 3)) {
+              float dv = acc[i][j][4 * q];
+#pragma unroll
+              for (int e = 1; e < 4; ++e) dv = (e == (m & 3)) ? acc[i][j][4 * q + e] : dv;
+              if constexpr (KIND == GEMM_GRAM) dv = s2 * dv;
+              else dv = p.b * drow[ii] + p.c * (dv + drow[ii] * drow[ii]);
+              dout[grow + 32 * i] = dv;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = (e == (m & 3)) ? 0.f : v[e];
+            }
+            const int ch = (wn * WN + 32 * j + 8 * q) >> 3;
+            uint2 w;
+            w.x = pack_bf2(v[0], v[1]);
+            w.y = pack_bf2(v[2], v[3]);
+            *reinterpret_cast<uint2*>(trow + ((ch ^ (r & 31)) << 4)) = w;
+          }
+      }
     }
     __syncthreads();
     auto tbyte = [&](int row, int col) __attribute__((always_inline)) {
@@ -534,7 +577,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     for (int itr = 0; itr < BM / ROWS_PER_IT; ++itr) {
       const int row = itr * ROWS_PER_IT + (tid >> 5);
       const u32x4 w = *reinterpret_cast<const u32x4*>(tbyte(row, ch * 8));
-      *reinterpret_cast<u32x4*>(d.Ao + (row0 + row) * rp + col0 + ch * 8) = w;
+      *reinterpret_cast<u32x4*>(out + (row0 + row) * rp + col0 + ch * 8) = w;
     }
     if (!diag) {
       // 16-lane group g reads tile rows R0 .. R0 + 7 (R0 = 32 rb + 8 g) of
@@ -552,7 +595,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
           const v4i16 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr, sc));
           const v4i16 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr + 4, sc));
           const u32x4 w = __builtin_bit_cast(u32x4, __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7));
-          *reinterpret_cast<u32x4*>(d.Ao + (col0 + C0 + li) * rp + row0 + R0) = w;
+          *reinterpret_cast<u32x4*>(out + (col0 + C0 + li) * rp + row0 + R0) = w;
         }
       }
     }
