@@ -447,9 +447,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     }
   }
 
-  const bool sym = (KIND != GEMM_APPLY);
-  const bool diag = sym && it.tm == it.tn;
-  const bool last = (KIND == GEMM_APPLY) && p.last;
+  const bool diag = (KIND != GEMM_APPLY) && it.tm == it.tn;  // Gram / square tile on the diagonal
   const float alpha = (p.iter == 0) ? *d.alpha : 1.0f;
   if constexpr (DIRECT) {
     // The whole 256 x 256 tile is staged once in LDS as bf16 (rows 0..127 in
@@ -601,176 +599,106 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     }
     return;
   }
-  // transposed outputs: square mirror tiles, and the parameter write of a
-  // wide matrix (the apply tile is a tile of X^T)
-  const bool need_t = (sym && !diag) || (last && !d.tall);
-
-  // Epilogue in four quarters of QM rows, staged alternately in s0 and s1.
-  constexpr int EPR = 8;                    // consecutive elements per thread
-  constexpr int TPRW = BN / EPR;            // threads per staged row (32)
-  constexpr int RPP = NTHREADS / TPRW;      // rows per pass
-  constexpr int NPASS = QM / RPP;
-  const int ec = (tid % TPRW) * EPR, er = tid / TPRW;
-  // Accumulator rows of MFMA blocks IB, IB+1 (one quarter) into the staging tile.
-  // acc[] needs static indices, so the block offset is a template parameter.
-  auto stage_acc = [&](float* T, auto ibc) __attribute__((always_inline)) {
-    constexpr int IB = decltype(ibc)::value;
+  // Last apply: the parameter write W <- decay W - lr s dscale X5, from X5^T
+  // tiles: a tall matrix's W is X^T itself (natural layout), a wide matrix's W
+  // is its transpose.  Four quarters of QM rows are staged in fp32, alternately
+  // in s0 and s1; the W pieces a thread updates are loaded before the quarter's
+  // barrier so their latency overlaps the staging.
+  if constexpr (KIND == GEMM_APPLY && !DIRECT) {
+    const bool wide = !d.tall;
+    const float dc = d.s * p.dscale;
+    const int64_t n = d.n;
+    WT* const Wb = reinterpret_cast<WT*>(d.W);
+    constexpr int EPR = 8;                    // consecutive elements per thread
+    constexpr int TPRW = BN / EPR;            // threads per staged row (32)
+    constexpr int RPP = NTHREADS / TPRW;      // rows per pass
+    constexpr int NPASS = QM / RPP;           // natural passes per quarter
+    constexpr int NPB = BN / (NTHREADS / 8);  // transposed passes per quarter
+    static_assert(NPASS == NPB, "one prefetch buffer serves both layouts");
+    static_assert(QM == 8 * EPR, "8 lanes per transposed row segment");
+    const int ec = (tid % TPRW) * EPR, er = tid / TPRW;
+    const int i0 = (tid & 7) * EPR;           // transposed: staged rows i0 .. i0 + 7
+    // Accumulator rows of MFMA blocks IB, IB+1 (one quarter) into the staging tile.
+    // acc[] needs static indices, so the block offset is a template parameter.
+    auto stage_acc = [&](float* T, auto ibc) __attribute__((always_inline)) {
+      constexpr int IB = decltype(ibc)::value;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < NI; ++j)
+        for (int j = 0; j < NI; ++j)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int r = i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-          const int c = wn * WN + j * 32 + (lane & 31);
-          T[tix(r, c)] = acc[IB + i][j][v];
-        }
-  };
-  constexpr int NQ = BM / QM;
-#pragma unroll 1
-  for (int h = 0; h < NQ; ++h) {
-    float* T = reinterpret_cast<float*>((h & 1) ? s1 : s0);
-    if (h >= 2) __syncthreads();  // quarter h-2 is fully consumed
-    if (wm == (h >> 1)) {
-      if (h & 1) stage_acc(T, std::integral_constant<int, 2>{});
-      else stage_acc(T, std::integral_constant<int, 0>{});
-    }
-    const int64_t qrow0 = row0 + h * QM;
-    // input of the natural-layout pass of the square: Ao
-    u32x4 xin[NPASS];  // packed bf16
-    if constexpr (KIND == GEMM_POLY) {
-#pragma unroll
-      for (int ps = 0; ps < NPASS; ++ps)
-        xin[ps] = *(gptr4)(d.Ao + (qrow0 + ps * RPP + er) * rp + col0 + ec);
-    }
-    auto xval = [&](int ps, int q) __attribute__((always_inline)) {
-      const uint32_t w = xin[ps][q >> 1];
-      return bf2f((q & 1) ? (w >> 16) : (w & 0xffffu));
+          for (int v = 0; v < 16; ++v) {
+            const int r = i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            const int c = wn * WN + j * 32 + (lane & 31);
+            T[tix(r, c)] = acc[IB + i][j][v];
+          }
     };
-    __syncthreads();
-    // ---- pass A: row-major; final values, natural-layout outputs ----
-#pragma unroll 2
-    for (int ps = 0; ps < NPASS; ++ps) {
-      const int r = ps * RPP + er;
-      const int64_t gi = qrow0 + r, gj = col0 + ec;
-      float v[EPR];
-      Vec<float>::load8(T + tix(r, ec), v);
-      if constexpr (KIND == GEMM_GRAM) {
-        // A = alpha^2 acc; the diagonal goes to dA (fp32), the rest to Ao (bf16)
-        const float s2 = alpha * alpha;
-#pragma unroll
-        for (int q = 0; q < EPR; ++q) {
-          v[q] *= s2;
-          if (diag && gi == gj + q) {
-            d.dA[gi] = v[q];
-            v[q] = 0.f;
-          }
-        }
-        Vec<uint16_t>::store8(d.Ao + gi * rp + gj, v);
-      } else if constexpr (KIND == GEMM_POLY) {
-        // A^2 = dA^2 + dA Ao + Ao dA + Ao Ao;  B = b A + c A^2
-        float dj[EPR];
-        Vec<float>::load8(d.dA + gj, dj);
-        const float di = d.dA[gi];
-#pragma unroll
-        for (int q = 0; q < EPR; ++q) {
-          const float ao = xval(ps, q);
-          if (diag && gi == gj + q) {
-            d.dB[gi] = p.b * di + p.c * (v[q] + di * di);
-            v[q] = 0.f;
-          } else {
-            v[q] = p.b * ao + p.c * (di * ao + ao * dj[q] + v[q]);
-          }
-        }
-        Vec<uint16_t>::store8(d.Bo + gi * rp + gj, v);
+    // W row / column of pass ps of quarter h, and whether the 8-wide fast path applies
+    auto wpos = [&](int h, int ps, int64_t& wr, int64_t& wc) __attribute__((always_inline)) {
+      if (wide) {
+        wr = col0 + ps * (NTHREADS / 8) + (tid >> 3);  // transposed row
+        wc = row0 + h * QM + i0;
       } else {
-        // X'^T = alpha (XT diag(a + dB) + XT Bo); the first term is in acc
+        wr = row0 + h * QM + ps * RPP + er;
+        wc = col0 + ec;
+      }
+      return wr < d.m && (n & 7) == 0 && wc + EPR <= n;
+    };
+    // the new value of 8 consecutive W elements from 8 NS5 outputs
+    auto wupdate = [&](int64_t wr, int64_t wc, bool fast, const float (&w)[EPR], const float (&v)[EPR])
+        __attribute__((always_inline)) {
+      if (wr >= d.m) return;
+      WT* W = Wb + wr * n;
+      float* Dp = d.D + wr * n;
+      if (fast) {
+        float wn8[EPR], dv[EPR];
 #pragma unroll
-        for (int q = 0; q < EPR; ++q) v[q] = alpha * v[q];
-        if (!last) {
-          Vec<uint16_t>::store8(XTo + gi * rp + gj, v);
-        } else if (d.tall) {
-          // tall: the tile of X^T is a tile of W (c x r = m x n)
-          const int64_t n = d.n;
-          if (gi < d.m) {
-            const float dc = d.s * p.dscale;
-            WT* W = reinterpret_cast<WT*>(d.W) + gi * n;
-            float* Dp = d.D + gi * n;
-            if ((n & 7) == 0 && gj + EPR <= n) {
-              float w[EPR], dv[EPR];
-              Vec<WT>::load8(W + gj, w);
+        for (int q = 0; q < EPR; ++q) {
+          dv[q] = dc * alpha * v[q];
+          wn8[q] = w[q] * p.decay - p.lr * dv[q];
+        }
+        Vec<WT>::store8(W + wc, wn8);
+        if (p.write_d) Vec<float>::store8(Dp + wc, dv);
+      } else {
 #pragma unroll
-              for (int q = 0; q < EPR; ++q) {
-                dv[q] = dc * v[q];
-                w[q] = w[q] * p.decay - p.lr * dv[q];
-              }
-              Vec<WT>::store8(W + gj, w);
-              if (p.write_d) Vec<float>::store8(Dp + gj, dv);
-            } else {
-#pragma unroll
-              for (int q = 0; q < EPR; ++q) {
-                if (gj + q < n) {
-                  const float dv = dc * v[q];
-                  Vec<WT>::store1(W + gj + q, Vec<WT>::load1(W + gj + q) * p.decay - p.lr * dv);
-                  if (p.write_d) Dp[gj + q] = dv;
-                }
-              }
-            }
+        for (int q = 0; q < EPR; ++q) {
+          if (wc + q < n) {
+            const float dv = dc * alpha * v[q];
+            Vec<WT>::store1(W + wc + q, Vec<WT>::load1(W + wc + q) * p.decay - p.lr * dv);
+            if (p.write_d) Dp[wc + q] = dv;
           }
         }
       }
-      if (need_t) Vec<float>::store8(T + tix(r, ec), v);  // same thread, same slots
-    }
-    if (!need_t) continue;
-    __syncthreads();
-    // ---- pass B: transposed outputs (mirror tiles, XT, tall parameter write) ----
-    // 8 lanes cover one transposed row segment of QM elements (one 128-byte
-    // line for bf16): thread -> tile column j = 32 pass + tid / 8, staged rows
-    // i0 .. i0+7 with i0 = 8 (tid % 8)
-    static_assert(QM == 8 * EPR, "8 lanes per transposed row segment");
-    const int i0 = (tid & 7) * EPR;
-#pragma unroll 2
-    for (int jp = 0; jp < BN; jp += NTHREADS / 8) {
-      const int j = jp + (tid >> 3);
-      const int64_t orow = col0 + j;  // transposed row
-      float v[EPR];
+    };
+    constexpr int NQ = BM / QM;
+#pragma unroll 1
+    for (int h = 0; h < NQ; ++h) {
+      float* T = reinterpret_cast<float*>((h & 1) ? s1 : s0);
+      if (h >= 2) __syncthreads();  // quarter h-2 is fully consumed
+      if (wm == (h >> 1)) {
+        if (h & 1) stage_acc(T, std::integral_constant<int, 2>{});
+        else stage_acc(T, std::integral_constant<int, 0>{});
+      }
+      float w[NPASS][EPR];
 #pragma unroll
-      for (int q = 0; q < EPR; ++q) v[q] = T[tix(i0 + q, j)];
-      const int64_t ocol = qrow0 + i0;  // transposed column start
-      if constexpr (KIND == GEMM_GRAM) {
-        Vec<uint16_t>::store8(d.Ao + orow * rp + ocol, v);
-      } else if constexpr (KIND == GEMM_POLY) {
-        Vec<uint16_t>::store8(d.Bo + orow * rp + ocol, v);
-      } else {
-        {
-          // wide: the transposed tile of X^T is a tile of W (r x c = m x n)
-          const int64_t n = d.n;
-          if (orow < d.m) {
-            const float dc = d.s * p.dscale;
-            WT* W = reinterpret_cast<WT*>(d.W) + orow * n;
-            float* Dp = d.D + orow * n;
-            if ((n & 7) == 0 && ocol + EPR <= n) {
-              float w[EPR], dv[EPR];
-              Vec<WT>::load8(W + ocol, w);
+      for (int ps = 0; ps < NPASS; ++ps) {
+        int64_t wr, wc;
+        if (wpos(h, ps, wr, wc)) Vec<WT>::load8(Wb + wr * n + wc, w[ps]);
+      }
+      __syncthreads();
 #pragma unroll
-              for (int q = 0; q < EPR; ++q) {
-                dv[q] = dc * v[q];
-                w[q] = w[q] * p.decay - p.lr * dv[q];
-              }
-              Vec<WT>::store8(W + ocol, w);
-              if (p.write_d) Vec<float>::store8(Dp + ocol, dv);
-            } else {
+      for (int ps = 0; ps < NPASS; ++ps) {
+        int64_t wr, wc;
+        const bool fast = wpos(h, ps, wr, wc);
+        float v[EPR];
+        if (wide) {
+          const int j = ps * (NTHREADS / 8) + (tid >> 3);
 #pragma unroll
-              for (int q = 0; q < EPR; ++q) {
-                if (ocol + q < n) {
-                  const float dv = dc * v[q];
-                  Vec<WT>::store1(W + ocol + q, Vec<WT>::load1(W + ocol + q) * p.decay - p.lr * dv);
-                  if (p.write_d) Dp[ocol + q] = dv;
-                }
-              }
-            }
-          }
+          for (int q = 0; q < EPR; ++q) v[q] = T[tix(i0 + q, j)];
+        } else {
+          Vec<float>::load8(T + tix(ps * RPP + er, ec), v);
         }
+        wupdate(wr, wc, fast, w[ps], v);
       }
     }
   }
