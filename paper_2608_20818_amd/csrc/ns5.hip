@@ -369,9 +369,14 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
       if constexpr (TN) fb[set][j] = rd_tn(b, tn_offb[j], ks);
       else fb[set][j] = *reinterpret_cast<const bf16x8*>(b + swz(brow + j * 32, ks * 2 + khalf));
     };
-    // loads at the start; the rest go one per DMA_SLOT-th sub-group over k-steps 0..2
-    constexpr int DMA0 = NDMA / 4, DMA_SLOT = (3 * MI) / (NDMA - DMA0);
-    static_assert((NDMA - DMA0) * DMA_SLOT == 3 * MI, "loads spread evenly over three k-steps");
+    // a quarter of the loads at the start, the rest spread over the sub-groups
+    // of the first DMA_KSTEPS k-steps (sub-group s issues loads
+    // [DMA0 + REM s / NS, DMA0 + REM (s + 1) / NS))
+#ifndef PRM_DMA_KSTEPS
+#define PRM_DMA_KSTEPS 2
+#endif
+    constexpr int DMA0 = NDMA / 4, REM = NDMA - DMA0, NS = PRM_DMA_KSTEPS * MI;
+    static_assert(PRM_DMA_KSTEPS >= 1 && PRM_DMA_KSTEPS <= 3, "loads must be issued before the last k-step");
     if (more) {
 #pragma unroll
       for (int q = 0; q < DMA0; ++q) dma1(nxt, kn, q);
@@ -387,8 +392,11 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
 #pragma unroll
       for (int i = 0; i < MI; ++i) {          // sub-group: row block i, NI MFMAs
         if (ks < 3) {
-          const int slot = ks * MI + i;
-          if (more && slot % DMA_SLOT == 0) dma1(nxt, kn, DMA0 + slot / DMA_SLOT);
+          if (ks < PRM_DMA_KSTEPS && more) {
+            const int slot = ks * MI + i;
+#pragma unroll
+            for (int q = DMA0 + REM * slot / NS; q < DMA0 + REM * (slot + 1) / NS; ++q) dma1(nxt, kn, q);
+          }
           rda(cs ^ 1, i, ks + 1);
           if (i < NI) rdb(cs ^ 1, i, ks + 1);
         }
