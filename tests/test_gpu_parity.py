@@ -76,6 +76,20 @@ def test_ragged_shapes_all_paths(t, wdt, gdt):
     check(res, rho, cfg, RAGGED, cfg.lr)
 
 
+# several 256 x 256 tiles per symmetric product with padding: tiles above the
+# diagonal and their mirrors (Gram, square), the fold stage pairs and the
+# transposed parameter write of the last apply
+MULTI_TILE = [(700, 2000), (1536, 520), (600, 600), (1300, 1800)]
+
+
+@pytest.mark.parametrize("t,wdt,gdt", [(0, 1, 1), (0, 0, 0), (1, 1, 1)])
+def test_multi_tile_symmetric_products(t, wdt, gdt):
+    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=wdt, grad_dtype=gdt)
+    rho, res = run_one_step(MULTI_TILE, cfg, t, workload_id=93)
+    assert rho == (1 if t == 0 else 0)
+    check(res, rho, cfg, MULTI_TILE, cfg.lr)
+
+
 @pytest.mark.parametrize("flag", ["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh"])
 @pytest.mark.parametrize("t", [0, 3])
 def test_variants(flag, t):
