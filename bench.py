@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--K", type=int, default=None, help="refresh period (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel attribution period")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the measured MFMA / HBM ceilings (libprm calibration probes)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 4 GiB device-to-device copy (HBM bandwidth and counter calibration)")
     return ap.parse_args()
@@ -292,6 +294,27 @@ def main():
         log(f"[bench] kernels: " + ", ".join(f"{k} {v['total_ms']:.2f}ms/{v['launches']}" for k, v in kernels.items() if v["launches"]))
 
     opt.close()
+    peaks = None
+    if not args.no_peaks:
+        # the ceilings the kernels can reach on this machine: a pure MFMA loop (it
+        # runs into the power limit, so its clock is below the nominal 2.4 GHz)
+        # and 16-byte streaming read / write / copy
+        mf = prm.peak_mfma(50000)
+        hb = prm.peak_hbm(4 << 30)
+        # a step that reads R and writes Wr bytes per element moves them at best
+        # at (R + Wr) / (R / read_rate + Wr / write_rate)
+        rb, wrb = gb + 4 + wb, 4 + wb
+        mix = (rb + wrb) / (rb / hb["read_gbs"] + wrb / hb["write_gbs"])
+        peaks = {"mfma_bf16_tflops": mf["tflops"], "mfma_clock_ghz": mf["clock_ghz"],
+                 "hbm_read_gbs": hb["read_gbs"], "hbm_write_gbs": hb["write_gbs"], "hbm_copy_gbs": hb["copy_gbs"],
+                 "hbm_rowwise_mix_gbs": mix, "rowwise_mix": f"{rb} B read + {wrb} B written per element"}
+        log(f"[bench] measured ceilings: MFMA {mf['tflops']:.0f} TFLOP/s at {mf['clock_ghz']:.2f} GHz, "
+            f"HBM read {hb['read_gbs']:.0f} / write {hb['write_gbs']:.0f} / copy {hb['copy_gbs']:.0f} GB/s")
+        for rf in (roofline, roofline_rw):
+            if rf is not None:
+                mp = mf["tflops"] if rf["bound"] == "mfma" else mix
+                rf["measured_peak"] = mp
+                rf["frac_of_measured"] = rf["achieved"] / mp
     cpu = None
     if not args.no_cpu_baseline:
         del W, M, G
@@ -323,6 +346,11 @@ def main():
         "rowwise_ms": T_rw,
         "refresh_mfma_frac": refresh_mfma_frac,
         "rowwise_hbm_frac": rowwise_hbm_frac,
+        "peaks_measured": peaks,
+        "refresh_mfma_frac_of_measured": (ns_flops / (T_ref * 1e-3) / (peaks["mfma_bf16_tflops"] * 1e12)
+                                          if ref and peaks else None),
+        "rowwise_hbm_frac_of_measured": (rw_bytes / (T_rw * 1e-3) / (peaks["hbm_rowwise_mix_gbs"] * 1e9)
+                                         if rw and peaks else None),
         "amortized_ms_by_K": ({str(k): (T_ref + (k - 1) * T_rw) / k for k in (1, 3, 5, 10)}
                               if ref and rw else None),
         "single_gpu_reduction_K3_vs_K1": ((T_ref - (T_ref + 2 * T_rw) / 3) / T_ref if ref and rw else None),

@@ -150,6 +150,28 @@ int prm_profile_read(prm_ctx* ctx, prm_kernel_stats* out, int32_t n);
  * context.  NULL is a no-op. */
 int prm_destroy(prm_ctx* ctx);
 
+/* Calibration probes (not part of the optimizer step).  They measure the
+ * ceilings the step's kernels are compared against, on the device current on
+ * the calling thread, with the instructions the step uses; each call
+ * synchronizes `hip_stream` and allocates and frees its own device buffers.
+ *
+ * prm_peak_mfma: sustained bf16 MFMA rate.  Every wave runs 8 independent
+ * 32x32x16 accumulator chains for `iters` iterations (1 <= iters <= 2^24; 16
+ * waves per compute unit, no memory traffic).  *tflops = executed FLOPs over
+ * the HIP-event time; *clock_ghz = the shader clock during the loop (shader
+ * cycles over 100 MHz reference ticks), which drops below the nominal
+ * 2.4 GHz when the power limit is reached.
+ *
+ * prm_peak_hbm: HBM stream rates over two buffers of `bytes` bytes each
+ * (>= 1 MiB, a multiple of 16): a read-only pass, a write-only pass and a copy,
+ * with 16-byte nontemporal accesses; the best of three timed repetitions, in
+ * GB/s of bytes moved (the copy counts reads and writes).
+ *
+ * Errors: PRM_EINVAL for NULL outputs or out-of-range sizes, PRM_ENOMEM when
+ * the buffers cannot be allocated, PRM_EHIP for a failed HIP call. */
+int prm_peak_mfma(void* hip_stream, int32_t iters, double* tflops, double* clock_ghz);
+int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* write_gbs, double* copy_gbs);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* prm_last_error(void);
 

@@ -88,6 +88,11 @@ def load() -> ctypes.CDLL:
     L.prm_destroy.restype = ctypes.c_int
     L.prm_last_error.argtypes = []
     L.prm_last_error.restype = ctypes.c_char_p
+    dp = ctypes.POINTER(ctypes.c_double)
+    L.prm_peak_mfma.argtypes = [P, ctypes.c_int32, dp, dp]
+    L.prm_peak_mfma.restype = ctypes.c_int
+    L.prm_peak_hbm.argtypes = [P, ctypes.c_uint64, dp, dp, dp]
+    L.prm_peak_hbm.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -126,6 +131,28 @@ def workspace_bytes(shapes, cfg: Config) -> int:
     return out.value
 
 
+def _stream_handle(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream().cuda_stream
+    return ctypes.c_void_p(int(stream) if stream else 0)
+
+
+def peak_mfma(iters: int = 20000, stream=None) -> dict:
+    """Sustained bf16 MFMA rate and shader clock (calibration; see prm.h)."""
+    t, g = ctypes.c_double(), ctypes.c_double()
+    _check(load().prm_peak_mfma(_stream_handle(stream), int(iters), ctypes.byref(t), ctypes.byref(g)))
+    return {"tflops": t.value, "clock_ghz": g.value}
+
+
+def peak_hbm(nbytes: int = 4 << 30, stream=None) -> dict:
+    """HBM read, write and copy rates in GB/s (calibration; see prm.h)."""
+    r, w, c = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(load().prm_peak_hbm(_stream_handle(stream), int(nbytes), ctypes.byref(r), ctypes.byref(w),
+                               ctypes.byref(c)))
+    return {"read_gbs": r.value, "write_gbs": w.value, "copy_gbs": c.value}
+
+
 def _ptr(x) -> int:
     return x if isinstance(x, int) else x.data_ptr()
 
@@ -144,14 +171,11 @@ class Optimizer:
     def __init__(self, shapes, cfg: Config | None = None, stream=None):
         self.shapes = [(int(m), int(n)) for m, n in shapes]
         self.cfg = cfg if cfg is not None else config_default()
-        if stream is None:
-            import torch
-            stream = torch.cuda.current_stream().cuda_stream
-        self.stream = stream
+        h = _stream_handle(stream)
+        self.stream = h.value or 0
         n, rows, cols = _shape_arrays(self.shapes)
         ctx = ctypes.c_void_p()
-        _check(load().prm_init(ctypes.byref(ctx), n, rows, cols, ctypes.byref(self.cfg),
-                               ctypes.c_void_p(int(stream) if stream else 0)))
+        _check(load().prm_init(ctypes.byref(ctx), n, rows, cols, ctypes.byref(self.cfg), h))
         self._ctx = ctx
 
     def _check_tensors(self, xs, dtype_name, what):

@@ -749,6 +749,92 @@ int prm_destroy(prm_ctx* c) {
   return rc;
 }
 
+int prm_peak_mfma(void* hip_stream, int32_t iters, double* tflops, double* clock_ghz) {
+  if (!tflops || !clock_ghz) return fail(PRM_EINVAL, "tflops and clock_ghz must not be NULL");
+  if (iters < 1 || iters > (1 << 24)) return fail(PRM_EINVAL, "iters must be in [1, 2^24] (got %d)", iters);
+  hipStream_t s = (hipStream_t)hip_stream;
+  int dev = 0, cus = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  const int blocks = 4 * cus;  // 16 waves per CU
+  float* sink = nullptr;
+  unsigned long long* clk = nullptr;
+  HIP_TRY(hipMalloc(&sink, (size_t)blocks * 256 * sizeof(float)));
+  if (hipMalloc(&clk, (size_t)blocks * 2 * sizeof(unsigned long long)) != hipSuccess) {
+    (void)hipFree(sink);
+    return fail(PRM_ENOMEM, "hipMalloc of the probe clocks failed");
+  }
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = PRM_OK;
+  std::vector<unsigned long long> h((size_t)blocks * 2);
+  float ms = 0.f;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
+      launch_probe_mfma(blocks, sink, clk, 64, s) != hipSuccess ||  // warm-up
+      hipEventRecord(e0, s) != hipSuccess || launch_probe_mfma(blocks, sink, clk, iters, s) != hipSuccess ||
+      hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+      hipEventElapsedTime(&ms, e0, e1) != hipSuccess ||
+      hipMemcpy(h.data(), clk, h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost) != hipSuccess)
+    rc = fail(PRM_EHIP, "MFMA probe failed: %s", hipGetErrorString(hipGetLastError()));
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  (void)hipFree(sink);
+  (void)hipFree(clk);
+  if (rc) return rc;
+  double cyc = 0, ref = 0;
+  for (int b = 0; b < blocks; ++b) { cyc += (double)h[2 * b]; ref += (double)h[2 * b + 1]; }
+  // 4 waves per block, 8 MFMAs of 32 x 32 x 16 (2 FLOPs per MAC) per iteration
+  const double flops = (double)blocks * 4 * (double)iters * 8 * (32.0 * 32 * 16 * 2);
+  *tflops = flops / (ms * 1e-3) / 1e12;
+  *clock_ghz = ref > 0 ? cyc / ref * 0.1 : 0.0;  // reference clock: 100 MHz
+  return PRM_OK;
+}
+
+int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* write_gbs, double* copy_gbs) {
+  if (!read_gbs || !write_gbs || !copy_gbs) return fail(PRM_EINVAL, "output pointers must not be NULL");
+  if (bytes < (1u << 20) || bytes % 16) return fail(PRM_EINVAL, "bytes must be >= 1 MiB and a multiple of 16");
+  hipStream_t s = (hipStream_t)hip_stream;
+  int dev = 0, cus = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  void *x = nullptr, *y = nullptr;
+  unsigned* sink = nullptr;
+  if (hipMalloc(&x, bytes) != hipSuccess || hipMalloc(&y, bytes) != hipSuccess ||
+      hipMalloc(&sink, 256) != hipSuccess) {
+    if (x) (void)hipFree(x);
+    if (y) (void)hipFree(y);
+    return fail(PRM_ENOMEM, "hipMalloc of 2 x %llu probe bytes failed", (unsigned long long)bytes);
+  }
+  const int64_t n16 = (int64_t)(bytes / 16);
+  const int blocks = 8 * cus;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = PRM_OK;
+  double* out[3] = {read_gbs, write_gbs, copy_gbs};
+  const double moved[3] = {(double)bytes, (double)bytes, 2.0 * (double)bytes};
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
+      launch_probe_stream(1, blocks, nullptr, x, n16, sink, s) != hipSuccess)  // defined contents of x
+    rc = fail(PRM_EHIP, "HBM probe setup failed");
+  for (int kind = 0; kind < 3 && rc == PRM_OK; ++kind) {
+    float best = 0.f;
+    for (int rep = 0; rep < 4 && rc == PRM_OK; ++rep) {  // first repetition is a warm-up
+      float ms = 0.f;
+      if (hipEventRecord(e0, s) != hipSuccess || launch_probe_stream(kind, blocks, x, y, n16, sink, s) != hipSuccess ||
+          hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+          hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+        rc = fail(PRM_EHIP, "HBM probe kernel %d failed: %s", kind, hipGetErrorString(hipGetLastError()));
+        break;
+      }
+      if (rep > 0 && (best == 0.f || ms < best)) best = ms;
+    }
+    if (rc == PRM_OK) *out[kind] = moved[kind] / (best * 1e-3) / 1e9;
+  }
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  (void)hipFree(x);
+  (void)hipFree(y);
+  (void)hipFree(sink);
+  return rc;
+}
+
 const char* prm_last_error(void) { return g_err.c_str(); }
 
 }  // extern "C"

@@ -103,6 +103,12 @@ enum GemmKind : int32_t { GEMM_GRAM = 0, GEMM_POLY = 1, GEMM_APPLY = 2 };
 hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item* items,
                           int32_t nitems, const NsParams& p, hipStream_t s);
 
+// calibration probes (probe.hip)
+hipError_t launch_probe_mfma(int blocks, float* sink, unsigned long long* clk, int iters, hipStream_t s);
+// kind 0: read x, 1: write y, 2: copy x -> y; n16 16-byte elements
+hipError_t launch_probe_stream(int kind, int blocks, const void* x, void* y, int64_t n16, unsigned* sink,
+                               hipStream_t s);
+
 // GEMM tile edge used by the NS5 kernels; rp and cp are multiples of it.
 constexpr int kNsTile = 256;
 // Prologue tile edge.

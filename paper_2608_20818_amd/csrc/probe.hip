@@ -1,0 +1,82 @@
+// Calibration probes: the sustained bf16 MFMA rate and the HBM stream rates of
+// the device, measured with the instructions the hot path uses (MFMA
+// 32x32x16 bf16; 16-byte vector loads and stores).  They are not part of the
+// optimizer step; bench.py reports the optimizer's rates against these
+// measured ceilings beside the spec figures.
+#include "prm_internal.h"
+
+namespace prm {
+
+typedef __bf16 pbf16x8 __attribute__((ext_vector_type(8)));
+typedef float pfloatx16 __attribute__((ext_vector_type(16)));
+
+// Every wave runs 8 independent accumulator chains, so the MFMA pipe never
+// waits on a result; operands stay in registers (no memory traffic).
+__global__ __launch_bounds__(256) void probe_mfma_kernel(float* sink, unsigned long long* clk, int iters) {
+  const int lane = threadIdx.x & 63;
+  pbf16x8 a, b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(0.001f * (float)(lane + e));
+    b[e] = (__bf16)(0.002f * (float)(lane - e));
+  }
+  pfloatx16 c[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) c[j][v] = 0.f;
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime(), r0 = __builtin_amdgcn_s_memrealtime();
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c[j], 0, 0, 0);
+  }
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime(), r1 = __builtin_amdgcn_s_memrealtime();
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s += c[j][v];
+  sink[blockIdx.x * 256 + threadIdx.x] = s;
+  if (threadIdx.x == 0) {
+    clk[2 * blockIdx.x] = t1 - t0;      // shader clock cycles
+    clk[2 * blockIdx.x + 1] = r1 - r0;  // 100 MHz reference ticks
+  }
+}
+
+typedef unsigned int pu32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void probe_read_kernel(const pu32x4* __restrict__ x, int64_t n, unsigned* sink) {
+  pu32x4 acc = {0u, 0u, 0u, 0u};
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    acc ^= __builtin_nontemporal_load(x + i);
+  if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9e3779b9u) sink[0] = 1u;  // keeps the loads
+}
+
+__global__ __launch_bounds__(256) void probe_write_kernel(pu32x4* __restrict__ y, int64_t n) {
+  const pu32x4 v = {1u, 2u, 3u, 4u};
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    __builtin_nontemporal_store(v, y + i);
+}
+
+__global__ __launch_bounds__(256) void probe_copy_kernel(const pu32x4* __restrict__ x, pu32x4* __restrict__ y,
+                                                         int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    __builtin_nontemporal_store(__builtin_nontemporal_load(x + i), y + i);
+}
+
+hipError_t launch_probe_mfma(int blocks, float* sink, unsigned long long* clk, int iters, hipStream_t s) {
+  probe_mfma_kernel<<<dim3(blocks), dim3(256), 0, s>>>(sink, clk, iters);
+  return hipGetLastError();
+}
+
+hipError_t launch_probe_stream(int kind, int blocks, const void* x, void* y, int64_t n16, unsigned* sink,
+                               hipStream_t s) {
+  switch (kind) {
+    case 0: probe_read_kernel<<<dim3(blocks), dim3(256), 0, s>>>((const pu32x4*)x, n16, sink); break;
+    case 1: probe_write_kernel<<<dim3(blocks), dim3(256), 0, s>>>((pu32x4*)y, n16); break;
+    default: probe_copy_kernel<<<dim3(blocks), dim3(256), 0, s>>>((const pu32x4*)x, (pu32x4*)y, n16); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace prm

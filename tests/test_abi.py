@@ -134,3 +134,13 @@ def test_null_context_calls_fail_cleanly():
     assert L.prm_profile_read(None, None, 0) == prm.PRM_EINVAL
     assert L.prm_destroy(None) == prm.PRM_OK
     assert L.prm_init(None, 0, None, None, None, None) == prm.PRM_EINVAL
+
+
+def test_calibration_probes_validate_before_touching_the_device():
+    L = prm.load()
+    d = ctypes.c_double()
+    assert L.prm_peak_mfma(None, 100, None, ctypes.byref(d)) == prm.PRM_EINVAL
+    assert L.prm_peak_mfma(None, 0, ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
+    assert L.prm_peak_hbm(None, 1 << 30, None, ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
+    assert L.prm_peak_hbm(None, 1000, ctypes.byref(d), ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
+    assert L.prm_last_error().decode() != ""
