@@ -166,9 +166,7 @@ constexpr int DMA_PER_WAVE = BM / 8 / NWAVES;           // 1 KB wave loads per o
 constexpr int NDMA = 2 * DMA_PER_WAVE;                  // wave loads per stage (both operands)
 constexpr int ROWS_PER_WAVE = BM / NWAVES;              // NT: tile rows one wave loads per operand
 constexpr int KROWS_PER_WAVE = BK / NWAVES;             // TN: k-rows one wave loads per operand
-constexpr int QM = 64;                                  // epilogue quarter rows
-constexpr int EPI_LD = BN;                              // fp32 words per staged row
-static_assert(QM * EPI_LD * 4 <= STAGE_BYTES, "quarter tile fits a stage buffer");
+static_assert(BM * BN * 2 <= 2 * STAGE_BYTES, "the bf16 epilogue tile fits the two stage buffers");
 
 // byte offset of 16-byte chunk `ch` of tile row `r`: XOR swizzle of the eight
 // 16-byte chunks of a row by (r / 2) % 8.  A row is 128 B, half of the 64 x 4 B
@@ -194,23 +192,16 @@ __device__ __forceinline__ int swz_tn(int r, int ch) { return r * TN_ROW_BYTES +
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16* lds_v4i16;
 
-// fp32 staging tile of the epilogue (QM x 256, no padding): column c of row r
-// is stored at c ^ (8 * ((r / 8) % 8)), which keeps aligned 8-column groups
-// contiguous (row-major pass) and makes the column pass, where 8 lanes read 8
-// row groups of one column, free of bank conflicts.
-__device__ __forceinline__ int tix(int r, int c) { return r * EPI_LD + (c ^ (((r >> 3) & 7) << 3)); }
 }  // namespace gemm
 
-// DIRECT (apply, every iteration but the last): the operands enter the MFMAs
-// swapped, so each lane accumulates four consecutive output columns of one
-// output row, and the bf16 result is stored straight from the accumulators
-// (8 bytes per lane and 32-column block) with no staging through LDS.
-template <int KIND, DType WD, bool DIRECT>
+// The operands enter the MFMAs swapped, so each lane accumulates four
+// consecutive output columns of one output row (see the epilogue).  WD is the
+// parameter type, used by the parameter write of the last apply.
+template <int KIND, DType WD>
 __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDesc* __restrict__ md,
                                                          const Item* __restrict__ items,
                                                          NsParams p) {
   using namespace gemm;
-  using WT = typename NsStore<WD>::T;
   __shared__ __attribute__((aligned(16))) char s0[STAGE_BYTES];
   __shared__ __attribute__((aligned(16))) char s1[STAGE_BYTES];
 
@@ -332,10 +323,8 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     return __builtin_bit_cast(bf16x8, f);
   };
   auto mfma = [&](const bf16x8& x, const bf16x8& y, floatx16& c) __attribute__((always_inline)) {
-    // DIRECT, the Gram and the square accumulate the transposed block:
-    // (P Q^T)^T = Q P^T
-    if constexpr (DIRECT || KIND != GEMM_APPLY) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y, x, c, 0, 0, 0);
-    else c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, c, 0, 0, 0);
+    // accumulates the transposed block: (P Q^T)^T = Q P^T
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y, x, c, 0, 0, 0);
   };
 
   // Compute one stage from `cur` while streaming stage `knext` (if >= 0) into
@@ -455,54 +444,23 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     }
   }
 
+  // ---- epilogue ----
+  // Final values are formed in registers, converted to bf16 and the whole
+  // 256 x 256 tile is staged once in LDS (rows 0..127 in s0, 128..255 in s1;
+  // 512 B per row, 16-byte chunk c of row r stored at c ^ (r % 32)).  It then
+  // leaves as 512-byte row segments and/or as its mirror: transposing reads
+  // (ds_read_b64_tr_b16) give each lane 8 consecutive tile rows of one tile
+  // column, i.e. 16 bytes of a row of the mirrored tile.
+  //   apply:        X'^T rows; at the last iteration the parameter write
+  //                 instead (rows for a tall matrix, whose W is X^T; the
+  //                 mirror for a wide one)
+  //   Gram, square: rows, plus the mirror above the diagonal.
+  // Lane L holds output row 32 i + L % 32 of its wave block and, for block
+  // column j and q = 0..3, the 4 columns 32 j + 8 q + 4 (L / 32) + 0..3.
   const bool diag = (KIND != GEMM_APPLY) && it.tm == it.tn;  // Gram / square tile on the diagonal
   const float alpha = (p.iter == 0) ? *d.alpha : 1.0f;
-  if constexpr (DIRECT) {
-    // The whole 256 x 256 tile is staged once in LDS as bf16 (rows 0..127 in
-    // s0, 128..255 in s1; 512 B per row, 16-byte chunk c of row r stored at
-    // c ^ (r % 32)), then written out in full 512-byte row segments.
-    // Lane L holds output row 32 i + L % 32 of its wave block and, for block
-    // column j and q = 0..3, the 4 columns 32 j + 8 q + 4 (L / 32) + 0..3.
-    char* T = wm ? s1 : s0;
-    const int hl = lane >> 5;
-#pragma unroll
-    for (int i = 0; i < MI; ++i) {
-      const int r = 32 * i + (lane & 31);
-      char* trow = T + r * 512 + 8 * hl;
-#pragma unroll
-      for (int j = 0; j < NI; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int ch = (wn * WN + 32 * j + 8 * q) >> 3;
-          uint2 w;
-          w.x = pack_bf2(alpha * acc[i][j][4 * q + 0], alpha * acc[i][j][4 * q + 1]);
-          w.y = pack_bf2(alpha * acc[i][j][4 * q + 2], alpha * acc[i][j][4 * q + 3]);
-          *reinterpret_cast<uint2*>(trow + ((ch ^ (r & 31)) << 4)) = w;
-        }
-    }
-    __syncthreads();
-    const int ch = tid & 31;
-    constexpr int ROWS_PER_IT = NTHREADS / 32;
-#pragma unroll 4
-    for (int it = 0; it < BM / ROWS_PER_IT; ++it) {
-      const int row = it * ROWS_PER_IT + (tid >> 5);
-      const char* src = (row < 128 ? s0 : s1) + (row & 127) * 512 + ((ch ^ (row & 31)) << 4);
-      const u32x4 w = *reinterpret_cast<const u32x4*>(src);
-      *reinterpret_cast<u32x4*>(XTo + (row0 + row) * rp + col0 + ch * 8) = w;
-    }
-    return;
-  }
-  if constexpr (KIND != GEMM_APPLY) {
-    // Gram: A = alpha^2 acc; the diagonal goes to dA (fp32), the rest to Ao.
-    // Square: A^2 = dA^2 + dA Ao + Ao dA + Ao Ao with acc = Ao Ao, and
-    // B = b A + c A^2; the diagonal goes to dB (fp32), the rest to Bo.
-    // The tile is staged once in LDS as bf16 (layout as for DIRECT), written as
-    // 512-byte row segments, and for a tile above the diagonal also as its
-    // mirror: transposing reads (ds_read_b64_tr_b16) give each lane 8
-    // consecutive tile rows of one tile column, i.e. 16 bytes of a row of the
-    // mirrored tile.
-    uint16_t* out = (KIND == GEMM_GRAM) ? d.Ao : d.Bo;
-    float* dout = (KIND == GEMM_GRAM) ? d.dA : d.dB;
+  const bool last = (KIND == GEMM_APPLY) && p.last;
+  {
     const float s2 = alpha * alpha;
     char* T = wm ? s1 : s0;
     const int hl = lane >> 5, m = lane & 31;
@@ -510,6 +468,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     // == L / 32, at q = (L % 32) / 8, element (L % 32) % 4
     const bool dlane = diag && wm == wn && ((m >> 2) & 1) == hl;
     const int64_t grow = row0 + wm * WM + m, gcol = col0 + wn * WN + 4 * hl;
+    float* dout = (KIND == GEMM_GRAM) ? d.dA : d.dB;
     // square: dA of this lane's columns (the same for every row block)
     float dcol[NI][4][4];
     if constexpr (KIND == GEMM_POLY) {
@@ -546,24 +505,33 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
           for (int q = 0; q < 4; ++q) {
             float v[4];
             if constexpr (KIND == GEMM_GRAM) {
+              // A = alpha^2 acc
 #pragma unroll
               for (int e = 0; e < 4; ++e) v[e] = s2 * acc[i][j][4 * q + e];
-            } else {
+            } else if constexpr (KIND == GEMM_POLY) {
+              // A^2 = dA^2 + dA Ao + Ao dA + Ao Ao;  B = b A + c A^2
               const uint2 w2 = ao[ii][j][q];
               const float a4[4] = {bf2f(w2.x & 0xffffu), bf2f(w2.x >> 16), bf2f(w2.y & 0xffffu), bf2f(w2.y >> 16)};
 #pragma unroll
               for (int e = 0; e < 4; ++e)
                 v[e] = p.c * acc[i][j][4 * q + e] + (p.b + p.c * (drow[ii] + dcol[j][q][e])) * a4[e];
+            } else {
+              // X'^T = alpha (XT diag(a + dB) + XT Bo); both terms are in acc
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = alpha * acc[i][j][4 * q + e];
             }
-            if (i == j && dlane && q == (m >> 3)) {
-              float dv = acc[i][j][4 * q];
+            if constexpr (KIND != GEMM_APPLY) {
+              if (i == j && dlane && q == (m >> 3)) {
+                // the diagonal goes to dA / dB (fp32), the bf16 tile keeps 0
+                float dv = acc[i][j][4 * q];
 #pragma unroll
-              for (int e = 1; e < 4; ++e) dv = (e == (m & 3)) ? acc[i][j][4 * q + e] : dv;
-              if constexpr (KIND == GEMM_GRAM) dv = s2 * dv;
-              else dv = p.b * drow[ii] + p.c * (dv + drow[ii] * drow[ii]);
-              dout[grow + 32 * i] = dv;
+                for (int e = 1; e < 4; ++e) dv = (e == (m & 3)) ? acc[i][j][4 * q + e] : dv;
+                if constexpr (KIND == GEMM_GRAM) dv = s2 * dv;
+                else dv = p.b * drow[ii] + p.c * (dv + drow[ii] * drow[ii]);
+                dout[grow + 32 * i] = dv;
 #pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = (e == (m & 3)) ? 0.f : v[e];
+                for (int e = 0; e < 4; ++e) v[e] = (e == (m & 3)) ? 0.f : v[e];
+              }
             }
             const int ch = (wn * WN + 32 * j + 8 * q) >> 3;
             uint2 w;
@@ -573,140 +541,72 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
           }
       }
     }
-    __syncthreads();
-    auto tbyte = [&](int row, int col) __attribute__((always_inline)) {
-      return (row < 128 ? s0 : s1) + (row & 127) * 512 + ((((col >> 3) ^ (row & 31))) << 4) + (col & 7) * 2;
-    };
+  }
+  __syncthreads();
+  auto tbyte = [&](int row, int col) __attribute__((always_inline)) {
+    return (row < 128 ? s0 : s1) + (row & 127) * 512 + ((((col >> 3) ^ (row & 31))) << 4) + (col & 7) * 2;
+  };
+  // last apply: W[wr][wc .. wc + 7] <- decay W - lr s dscale x, x = 8 bf16 outputs
+  auto wupdate = [&](int64_t wr, int64_t wc, const u32x4& x) __attribute__((always_inline)) {
+    using WT = typename NsStore<WD>::T;
+    if (wr >= d.m) return;
+    const int64_t n = d.n;
+    const float dc = d.s * p.dscale;
+    WT* W = reinterpret_cast<WT*>(d.W) + wr * n;
+    float* Dp = d.D + wr * n;
+    float dv[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      dv[2 * q] = dc * bf2f(x[q] & 0xffffu);
+      dv[2 * q + 1] = dc * bf2f(x[q] >> 16);
+    }
+    if ((n & 7) == 0 && wc + 8 <= n) {
+      float w8[8];
+      Vec<WT>::load8(W + wc, w8);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) w8[q] = w8[q] * p.decay - p.lr * dv[q];
+      Vec<WT>::store8(W + wc, w8);
+      if (p.write_d) Vec<float>::store8(Dp + wc, dv);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (wc + q < n) {
+          Vec<WT>::store1(W + wc + q, Vec<WT>::load1(W + wc + q) * p.decay - p.lr * dv[q]);
+          if (p.write_d) Dp[wc + q] = dv[q];
+        }
+      }
+    }
+  };
+  uint16_t* const out = (KIND == GEMM_GRAM) ? d.Ao : (KIND == GEMM_POLY) ? d.Bo : XTo;
+  if (!last || d.tall) {
     const int ch = tid & 31;
     constexpr int ROWS_PER_IT = NTHREADS / 32;
 #pragma unroll 4
     for (int itr = 0; itr < BM / ROWS_PER_IT; ++itr) {
       const int row = itr * ROWS_PER_IT + (tid >> 5);
       const u32x4 w = *reinterpret_cast<const u32x4*>(tbyte(row, ch * 8));
-      *reinterpret_cast<u32x4*>(out + (row0 + row) * rp + col0 + ch * 8) = w;
+      if (!last) *reinterpret_cast<u32x4*>(out + (row0 + row) * rp + col0 + ch * 8) = w;
+      else wupdate(row0 + row, col0 + ch * 8, w);  // tall: the tile of X^T is a tile of W
     }
-    if (!diag) {
-      // 16-lane group g reads tile rows R0 .. R0 + 7 (R0 = 32 rb + 8 g) of
-      // columns C0 .. C0 + 15; source lane 4 a + b of the group points at
-      // row R0 + a (+4), columns C0 + 4 b .. +3
-      const int g = lane >> 4, li = lane & 15;
-      constexpr int CB = BN / 16 / NWAVES;  // 16-column blocks per wave
-#pragma unroll 2
-      for (int cb = 0; cb < CB; ++cb) {
-        const int C0 = (wave * CB + cb) * 16;
-#pragma unroll 4
-        for (int rb = 0; rb < BM / 32; ++rb) {
-          const int R0 = 32 * rb + 8 * g;
-          const int sr = R0 + (li >> 2), sc = C0 + 4 * (li & 3);
-          const v4i16 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr, sc));
-          const v4i16 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr + 4, sc));
-          const u32x4 w = __builtin_bit_cast(u32x4, __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7));
-          *reinterpret_cast<u32x4*>(out + (col0 + C0 + li) * rp + row0 + R0) = w;
-        }
-      }
-    }
-    return;
   }
-  // Last apply: the parameter write W <- decay W - lr s dscale X5, from X5^T
-  // tiles: a tall matrix's W is X^T itself (natural layout), a wide matrix's W
-  // is its transpose.  Four quarters of QM rows are staged in fp32, alternately
-  // in s0 and s1; the W pieces a thread updates are loaded before the quarter's
-  // barrier so their latency overlaps the staging.
-  if constexpr (KIND == GEMM_APPLY && !DIRECT) {
-    const bool wide = !d.tall;
-    const float dc = d.s * p.dscale;
-    const int64_t n = d.n;
-    WT* const Wb = reinterpret_cast<WT*>(d.W);
-    constexpr int EPR = 8;                    // consecutive elements per thread
-    constexpr int TPRW = BN / EPR;            // threads per staged row (32)
-    constexpr int RPP = NTHREADS / TPRW;      // rows per pass
-    constexpr int NPASS = QM / RPP;           // natural passes per quarter
-    constexpr int NPB = BN / (NTHREADS / 8);  // transposed passes per quarter
-    static_assert(NPASS == NPB, "one prefetch buffer serves both layouts");
-    static_assert(QM == 8 * EPR, "8 lanes per transposed row segment");
-    const int ec = (tid % TPRW) * EPR, er = tid / TPRW;
-    const int i0 = (tid & 7) * EPR;           // transposed: staged rows i0 .. i0 + 7
-    // Accumulator rows of MFMA blocks IB, IB+1 (one quarter) into the staging tile.
-    // acc[] needs static indices, so the block offset is a template parameter.
-    auto stage_acc = [&](float* T, auto ibc) __attribute__((always_inline)) {
-      constexpr int IB = decltype(ibc)::value;
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int r = i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-            const int c = wn * WN + j * 32 + (lane & 31);
-            T[tix(r, c)] = acc[IB + i][j][v];
-          }
-    };
-    // W row / column of pass ps of quarter h, and whether the 8-wide fast path applies
-    auto wpos = [&](int h, int ps, int64_t& wr, int64_t& wc) __attribute__((always_inline)) {
-      if (wide) {
-        wr = col0 + ps * (NTHREADS / 8) + (tid >> 3);  // transposed row
-        wc = row0 + h * QM + i0;
-      } else {
-        wr = row0 + h * QM + ps * RPP + er;
-        wc = col0 + ec;
-      }
-      return wr < d.m && (n & 7) == 0 && wc + EPR <= n;
-    };
-    // the new value of 8 consecutive W elements from 8 NS5 outputs
-    auto wupdate = [&](int64_t wr, int64_t wc, bool fast, const float (&w)[EPR], const float (&v)[EPR])
-        __attribute__((always_inline)) {
-      if (wr >= d.m) return;
-      WT* W = Wb + wr * n;
-      float* Dp = d.D + wr * n;
-      if (fast) {
-        float wn8[EPR], dv[EPR];
-#pragma unroll
-        for (int q = 0; q < EPR; ++q) {
-          dv[q] = dc * alpha * v[q];
-          wn8[q] = w[q] * p.decay - p.lr * dv[q];
-        }
-        Vec<WT>::store8(W + wc, wn8);
-        if (p.write_d) Vec<float>::store8(Dp + wc, dv);
-      } else {
-#pragma unroll
-        for (int q = 0; q < EPR; ++q) {
-          if (wc + q < n) {
-            const float dv = dc * alpha * v[q];
-            Vec<WT>::store1(W + wc + q, Vec<WT>::load1(W + wc + q) * p.decay - p.lr * dv);
-            if (p.write_d) Dp[wc + q] = dv;
-          }
-        }
-      }
-    };
-    constexpr int NQ = BM / QM;
-#pragma unroll 1
-    for (int h = 0; h < NQ; ++h) {
-      float* T = reinterpret_cast<float*>((h & 1) ? s1 : s0);
-      if (h >= 2) __syncthreads();  // quarter h-2 is fully consumed
-      if (wm == (h >> 1)) {
-        if (h & 1) stage_acc(T, std::integral_constant<int, 2>{});
-        else stage_acc(T, std::integral_constant<int, 0>{});
-      }
-      float w[NPASS][EPR];
-#pragma unroll
-      for (int ps = 0; ps < NPASS; ++ps) {
-        int64_t wr, wc;
-        if (wpos(h, ps, wr, wc)) Vec<WT>::load8(Wb + wr * n + wc, w[ps]);
-      }
-      __syncthreads();
-#pragma unroll
-      for (int ps = 0; ps < NPASS; ++ps) {
-        int64_t wr, wc;
-        const bool fast = wpos(h, ps, wr, wc);
-        float v[EPR];
-        if (wide) {
-          const int j = ps * (NTHREADS / 8) + (tid >> 3);
-#pragma unroll
-          for (int q = 0; q < EPR; ++q) v[q] = T[tix(i0 + q, j)];
-        } else {
-          Vec<float>::load8(T + tix(ps * RPP + er, ec), v);
-        }
-        wupdate(wr, wc, fast, w[ps], v);
+  if ((KIND != GEMM_APPLY && !diag) || (last && !d.tall)) {
+    // 16-lane group g reads tile rows R0 .. R0 + 7 (R0 = 32 rb + 8 g) of
+    // columns C0 .. C0 + 15; source lane 4 a + b of the group points at
+    // row R0 + a (+4), columns C0 + 4 b .. +3
+    const int g = lane >> 4, li = lane & 15;
+    constexpr int CB = BN / 16 / NWAVES;  // 16-column blocks per wave
+#pragma unroll 2
+    for (int cb = 0; cb < CB; ++cb) {
+      const int C0 = (wave * CB + cb) * 16;
+#pragma unroll 4
+      for (int rb = 0; rb < BM / 32; ++rb) {
+        const int R0 = 32 * rb + 8 * g;
+        const int sr = R0 + (li >> 2), sc = C0 + 4 * (li & 3);
+        const v4i16 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr, sc));
+        const v4i16 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr + 4, sc));
+        const u32x4 w = __builtin_bit_cast(u32x4, __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7));
+        if (!last) *reinterpret_cast<u32x4*>(out + (col0 + C0 + li) * rp + row0 + R0) = w;
+        else wupdate(col0 + C0 + li, row0 + R0, w);  // wide: the mirror of the X^T tile is a tile of W
       }
     }
   }
@@ -735,12 +635,11 @@ hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item
   if (nitems <= 0) return hipSuccess;
   dim3 g(nitems), b(gemm::NTHREADS);
   switch (kind) {
-    case GEMM_GRAM: ns_gemm_kernel<GEMM_GRAM, BF16, false><<<g, b, 0, s>>>(md, items, p); break;
-    case GEMM_POLY: ns_gemm_kernel<GEMM_POLY, BF16, false><<<g, b, 0, s>>>(md, items, p); break;
+    case GEMM_GRAM: ns_gemm_kernel<GEMM_GRAM, BF16><<<g, b, 0, s>>>(md, items, p); break;
+    case GEMM_POLY: ns_gemm_kernel<GEMM_POLY, BF16><<<g, b, 0, s>>>(md, items, p); break;
     case GEMM_APPLY:
-      if (!p.last) ns_gemm_kernel<GEMM_APPLY, BF16, true><<<g, b, 0, s>>>(md, items, p);
-      else if (wt == BF16) ns_gemm_kernel<GEMM_APPLY, BF16, false><<<g, b, 0, s>>>(md, items, p);
-      else ns_gemm_kernel<GEMM_APPLY, F32, false><<<g, b, 0, s>>>(md, items, p);
+      if (wt == BF16) ns_gemm_kernel<GEMM_APPLY, BF16><<<g, b, 0, s>>>(md, items, p);
+      else ns_gemm_kernel<GEMM_APPLY, F32><<<g, b, 0, s>>>(md, items, p);
       break;
     default: return hipErrorInvalidValue;
   }
