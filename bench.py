@@ -298,18 +298,24 @@ def main():
     if not args.no_peaks:
         # the ceilings the kernels can reach on this machine: a pure MFMA loop (it
         # runs into the power limit, so its clock is below the nominal 2.4 GHz)
-        # and 16-byte streaming read / write / copy
+        # and 16-byte streaming read / write / copy, plus a pass with the
+        # row-wise step's own element traffic (bf16 G, f32 M, bf16 W)
         mf = prm.peak_mfma(50000)
         hb = prm.peak_hbm(4 << 30)
-        # a step that reads R and writes Wr bytes per element moves them at best
-        # at (R + Wr) / (R / read_rate + Wr / write_rate)
         rb, wrb = gb + 4 + wb, 4 + wb
-        mix = (rb + wrb) / (rb / hb["read_gbs"] + wrb / hb["write_gbs"])
+        if (gb, wb) == (2, 2):
+            mix = hb["rowwise_gbs"]
+        else:
+            # other dtypes: R read and Wr written bytes per element move at
+            # best at (R + Wr) / (R / read_rate + Wr / write_rate)
+            mix = (rb + wrb) / (rb / hb["read_gbs"] + wrb / hb["write_gbs"])
         peaks = {"mfma_bf16_tflops": mf["tflops"], "mfma_clock_ghz": mf["clock_ghz"],
                  "hbm_read_gbs": hb["read_gbs"], "hbm_write_gbs": hb["write_gbs"], "hbm_copy_gbs": hb["copy_gbs"],
+                 "hbm_rowwise_probe_gbs": hb["rowwise_gbs"],
                  "hbm_rowwise_mix_gbs": mix, "rowwise_mix": f"{rb} B read + {wrb} B written per element"}
         log(f"[bench] measured ceilings: MFMA {mf['tflops']:.0f} TFLOP/s at {mf['clock_ghz']:.2f} GHz, "
-            f"HBM read {hb['read_gbs']:.0f} / write {hb['write_gbs']:.0f} / copy {hb['copy_gbs']:.0f} GB/s")
+            f"HBM read {hb['read_gbs']:.0f} / write {hb['write_gbs']:.0f} / copy {hb['copy_gbs']:.0f} / "
+            f"row-wise traffic {hb['rowwise_gbs']:.0f} GB/s")
         for rf in (roofline, roofline_rw):
             if rf is not None:
                 mp = mf["tflops"] if rf["bound"] == "mfma" else mix

@@ -164,13 +164,18 @@ int prm_destroy(prm_ctx* ctx);
  *
  * prm_peak_hbm: HBM stream rates over two buffers of `bytes` bytes each
  * (>= 1 MiB, a multiple of 16): a read-only pass, a write-only pass and a copy,
- * with 16-byte nontemporal accesses; the best of three timed repetitions, in
- * GB/s of bytes moved (the copy counts reads and writes).
+ * with one 16-byte nontemporal access per thread, and a pass with the
+ * row-wise step's element traffic (bf16 gradient, fp32 momentum and bf16
+ * weight read, momentum and weight written: 14 bytes per element, bytes/4
+ * elements, each access instruction contiguous across a wave).  Each rate is
+ * the best of three timed repetitions, in GB/s of bytes moved (reads plus
+ * writes).
  *
  * Errors: PRM_EINVAL for NULL outputs or out-of-range sizes, PRM_ENOMEM when
  * the buffers cannot be allocated, PRM_EHIP for a failed HIP call. */
 int prm_peak_mfma(void* hip_stream, int32_t iters, double* tflops, double* clock_ghz);
-int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* write_gbs, double* copy_gbs);
+int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* write_gbs, double* copy_gbs,
+                 double* rowwise_gbs);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* prm_last_error(void);

@@ -91,7 +91,7 @@ def load() -> ctypes.CDLL:
     dp = ctypes.POINTER(ctypes.c_double)
     L.prm_peak_mfma.argtypes = [P, ctypes.c_int32, dp, dp]
     L.prm_peak_mfma.restype = ctypes.c_int
-    L.prm_peak_hbm.argtypes = [P, ctypes.c_uint64, dp, dp, dp]
+    L.prm_peak_hbm.argtypes = [P, ctypes.c_uint64, dp, dp, dp, dp]
     L.prm_peak_hbm.restype = ctypes.c_int
     _lib = L
     return L
@@ -146,11 +146,11 @@ def peak_mfma(iters: int = 20000, stream=None) -> dict:
 
 
 def peak_hbm(nbytes: int = 4 << 30, stream=None) -> dict:
-    """HBM read, write and copy rates in GB/s (calibration; see prm.h)."""
-    r, w, c = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    """HBM read, write, copy and row-wise-traffic rates in GB/s (calibration; see prm.h)."""
+    r, w, c, x = ctypes.c_double(), ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
     _check(load().prm_peak_hbm(_stream_handle(stream), int(nbytes), ctypes.byref(r), ctypes.byref(w),
-                               ctypes.byref(c)))
-    return {"read_gbs": r.value, "write_gbs": w.value, "copy_gbs": c.value}
+                               ctypes.byref(c), ctypes.byref(x)))
+    return {"read_gbs": r.value, "write_gbs": w.value, "copy_gbs": c.value, "rowwise_gbs": x.value}
 
 
 def _ptr(x) -> int:

@@ -789,8 +789,9 @@ int prm_peak_mfma(void* hip_stream, int32_t iters, double* tflops, double* clock
   return PRM_OK;
 }
 
-int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* write_gbs, double* copy_gbs) {
-  if (!read_gbs || !write_gbs || !copy_gbs) return fail(PRM_EINVAL, "output pointers must not be NULL");
+int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* write_gbs, double* copy_gbs,
+                 double* rowwise_gbs) {
+  if (!read_gbs || !write_gbs || !copy_gbs || !rowwise_gbs) return fail(PRM_EINVAL, "output pointers must not be NULL");
   if (bytes < (1u << 20) || bytes % 16) return fail(PRM_EINVAL, "bytes must be >= 1 MiB and a multiple of 16");
   hipStream_t s = (hipStream_t)hip_stream;
   int dev = 0, cus = 0;
@@ -805,19 +806,31 @@ int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* wri
     return fail(PRM_ENOMEM, "hipMalloc of 2 x %llu probe bytes failed", (unsigned long long)bytes);
   }
   const int64_t n16 = (int64_t)(bytes / 16);
-  const int blocks = 8 * cus;
+  // one 16-byte element per thread: the dispatcher then walks the buffers in
+  // address order, which streams faster than a few grid-striding blocks
+  const int64_t nb = (n16 + 255) / 256;
+  if (nb > (int64_t)INT32_MAX) {
+    (void)hipFree(x);
+    (void)hipFree(y);
+    (void)hipFree(sink);
+    return fail(PRM_EINVAL, "bytes too large for one probe grid");
+  }
+  (void)cus;
+  // the row-wise pass: pieces of 4 elements (16 bytes of x), 512 per block
+  const int grid[4] = {(int)nb, (int)nb, (int)nb, (int)((n16 + 511) / 512)};
+  const int64_t count[4] = {n16, n16, n16, n16};
   hipEvent_t e0 = nullptr, e1 = nullptr;
   int rc = PRM_OK;
-  double* out[3] = {read_gbs, write_gbs, copy_gbs};
-  const double moved[3] = {(double)bytes, (double)bytes, 2.0 * (double)bytes};
+  double* out[4] = {read_gbs, write_gbs, copy_gbs, rowwise_gbs};
+  const double moved[4] = {(double)bytes, (double)bytes, 2.0 * (double)bytes, 4.0 * 14.0 * (double)n16};
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
-      launch_probe_stream(1, blocks, nullptr, x, n16, sink, s) != hipSuccess)  // defined contents of x
+      launch_probe_stream(1, grid[1], nullptr, x, n16, sink, s) != hipSuccess)  // defined contents of x
     rc = fail(PRM_EHIP, "HBM probe setup failed");
-  for (int kind = 0; kind < 3 && rc == PRM_OK; ++kind) {
+  for (int kind = 0; kind < 4 && rc == PRM_OK; ++kind) {
     float best = 0.f;
     for (int rep = 0; rep < 4 && rc == PRM_OK; ++rep) {  // first repetition is a warm-up
       float ms = 0.f;
-      if (hipEventRecord(e0, s) != hipSuccess || launch_probe_stream(kind, blocks, x, y, n16, sink, s) != hipSuccess ||
+      if (hipEventRecord(e0, s) != hipSuccess || launch_probe_stream(kind, grid[kind], x, y, count[kind], sink, s) != hipSuccess ||
           hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
           hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
         rc = fail(PRM_EHIP, "HBM probe kernel %d failed: %s", kind, hipGetErrorString(hipGetLastError()));

@@ -64,6 +64,36 @@ __global__ __launch_bounds__(256) void probe_copy_kernel(const pu32x4* __restric
     __builtin_nontemporal_store(__builtin_nontemporal_load(x + i), y + i);
 }
 
+// The row-wise step's element traffic: per element a bf16 gradient, an fp32
+// momentum and a bf16 weight are read, the momentum and the weight written
+// back (8 + 6 bytes).  Pieces of 4 elements: the momentum lives in x (16 bytes
+// a piece), gradient and weight share y (8 + 8).  Each thread takes pieces
+// p and p + 256 of its block's 512, so every access instruction covers one
+// contiguous span per wave; a thread that instead owns 32 contiguous momentum
+// bytes, written by two stores issued far apart, leaves half-written lines in
+// L2 and runs at about 60% of this rate.
+typedef unsigned int pu32x2 __attribute__((ext_vector_type(2)));
+__global__ __launch_bounds__(256) void probe_rowwise_kernel(pu32x4* __restrict__ x, pu32x4* __restrict__ y,
+                                                            int64_t npieces) {
+  pu32x2* G = reinterpret_cast<pu32x2*>(y);
+  pu32x2* W = G + npieces;
+  const int64_t p0 = (int64_t)blockIdx.x * 512 + threadIdx.x;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int64_t p = p0 + 256 * h;
+    if (p < npieces) {
+      const pu32x2 g = __builtin_nontemporal_load(G + p);
+      pu32x4 m = __builtin_nontemporal_load(x + p);
+      pu32x2 w = __builtin_nontemporal_load(W + p);
+      m.xy += g;
+      m.zw ^= g;
+      w += m.xy ^ m.zw;
+      __builtin_nontemporal_store(m, x + p);
+      __builtin_nontemporal_store(w, W + p);
+    }
+  }
+}
+
 hipError_t launch_probe_mfma(int blocks, float* sink, unsigned long long* clk, int iters, hipStream_t s) {
   probe_mfma_kernel<<<dim3(blocks), dim3(256), 0, s>>>(sink, clk, iters);
   return hipGetLastError();
@@ -74,7 +104,8 @@ hipError_t launch_probe_stream(int kind, int blocks, const void* x, void* y, int
   switch (kind) {
     case 0: probe_read_kernel<<<dim3(blocks), dim3(256), 0, s>>>((const pu32x4*)x, n16, sink); break;
     case 1: probe_write_kernel<<<dim3(blocks), dim3(256), 0, s>>>((pu32x4*)y, n16); break;
-    default: probe_copy_kernel<<<dim3(blocks), dim3(256), 0, s>>>((const pu32x4*)x, (pu32x4*)y, n16); break;
+    case 2: probe_copy_kernel<<<dim3(blocks), dim3(256), 0, s>>>((const pu32x4*)x, (pu32x4*)y, n16); break;
+    default: probe_rowwise_kernel<<<dim3(blocks), dim3(256), 0, s>>>((pu32x4*)x, (pu32x4*)y, n16); break;
   }
   return hipGetLastError();
 }

@@ -141,6 +141,7 @@ def test_calibration_probes_validate_before_touching_the_device():
     d = ctypes.c_double()
     assert L.prm_peak_mfma(None, 100, None, ctypes.byref(d)) == prm.PRM_EINVAL
     assert L.prm_peak_mfma(None, 0, ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
-    assert L.prm_peak_hbm(None, 1 << 30, None, ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
-    assert L.prm_peak_hbm(None, 1000, ctypes.byref(d), ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
+    assert L.prm_peak_hbm(None, 1 << 30, None, ctypes.byref(d), ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
+    assert L.prm_peak_hbm(None, 1 << 30, ctypes.byref(d), ctypes.byref(d), ctypes.byref(d), None) == prm.PRM_EINVAL
+    assert L.prm_peak_hbm(None, 1000, ctypes.byref(d), ctypes.byref(d), ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
     assert L.prm_last_error().decode() != ""

@@ -26,5 +26,5 @@ def test_peak_mfma_plausible():
 def test_peak_hbm_plausible():
     r = prm.peak_hbm(256 << 20)
     print(r, flush=True)
-    for k in ("read_gbs", "write_gbs", "copy_gbs"):
+    for k in ("read_gbs", "write_gbs", "copy_gbs", "rowwise_gbs"):
         assert 500.0 < r[k] < 8500.0, (k, r[k])
