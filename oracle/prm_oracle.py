@@ -37,6 +37,19 @@ reason, in the design notes of the repository):
 * weight decay      always uses eta_t (not gamma*eta_t), as eq.
                     (periodic-direction) writes it.
 
+Auxiliary AdamW group (the non-matrix parameters: Sec. 2, "Muon" setup, and
+App. "Optimizer and Training Hyperparameters" -- biases, normalization and
+other non-matrix parameters stay on AdamW with decoupled weight decay;
+optimizer-hyperparameter table: LR 1e-4, betas (0.9, 0.95), eps 1e-8, weight
+decay 0.01).  The paper cites AdamW (decoupled weight decay) without writing
+it out; ``adamw_step`` follows that method as published:
+
+* moments           m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2
+* bias correction   m^ = m / (1 - beta1^t), v^ = v / (1 - beta2^t), t >= 1 the
+                    update count including this one
+* parameter write   p <- p - eta (m^ / (sqrt(v^) + eps) + lambda p)
+                    (decay uses the old p and is not normalized by v^)
+
 Also provided for the pins (not part of the method):
 ``ns5_closed_form`` (U phi5(S/(||M||_F+eps)) V^T, from an SVD), ``polar``
 (U V^T) and ``ns5_rows_closed_form`` (selected oriented rows of NS5 through an
@@ -274,6 +287,53 @@ def step(Ws, Ms, Gs, t: int, cfg: PRMConfig, lr: float | None = None):
     if rho is None:
         rho = 0 if cfg.never_refresh else refresh_indicator(t, cfg.K)
     return out_W, out_M, out_D, rho
+
+
+# --------------------------------------------------------------------------
+# auxiliary AdamW group
+# --------------------------------------------------------------------------
+@dataclass
+class AdamWConfig:
+    """Aux AdamW settings of the optimizer-hyperparameter table (LR 1e-4,
+    betas (0.9, 0.95)) and its caption (eps 1e-8, weight decay 0.01)."""
+    lr: float = 1e-4
+    beta1: float = 0.9
+    beta2: float = 0.95
+    eps: float = 1e-8
+    wd: float = 0.01
+
+
+def adamw_step(p: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray, t: int,
+               cfg: AdamWConfig, lr: float | None = None):
+    """One AdamW update of one tensor.  Returns (p_new, m_new, v_new).
+
+    Adam's first and second moment estimates with their bias corrections,
+    then the decoupled weight-decay write (the update the paper keeps for its
+    non-matrix parameters, App. "Optimizer and Training Hyperparameters").
+    ``t`` is the 1-based number of this update.
+    """
+    if t < 1:
+        raise ValueError("t must be >= 1")
+    eta = cfg.lr if lr is None else lr
+    p = np.asarray(p, dtype=np.float64)
+    g = np.asarray(g, dtype=np.float64)
+    m = np.asarray(m, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    # first and second raw moment estimates
+    m_new = cfg.beta1 * m + (1.0 - cfg.beta1) * g
+    v_new = cfg.beta2 * v + (1.0 - cfg.beta2) * (g * g)
+    # bias-corrected estimates
+    m_hat = m_new / (1.0 - cfg.beta1 ** t)
+    v_hat = v_new / (1.0 - cfg.beta2 ** t)
+    # decoupled weight decay on the old parameter, plus the normalized step
+    p_new = p - eta * (m_hat / (np.sqrt(v_hat) + cfg.eps) + cfg.wd * p)
+    return p_new, m_new, v_new
+
+
+def adamw_bytes_per_element(param_bytes: int, grad_bytes: int) -> int:
+    """Algorithmic HBM bytes of one AdamW element: p, g, m, v read once; p, m, v
+    written once (m and v fp32)."""
+    return 2 * param_bytes + grad_bytes + 2 * 4 + 2 * 4
 
 
 # --------------------------------------------------------------------------

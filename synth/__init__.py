@@ -14,6 +14,14 @@ momenta with the shapes and value distributions of the workloads:
   U diag((1 + beta + beta^2) s) V^T + 0.01 sqrt(1 + beta^2 + beta^4) N(0, 1);
   it is drawn directly from that distribution (one seeded draw).
 
+The auxiliary (non-matrix) group that AdamW updates -- biases, norm scales and
+shifts, embedders -- is a list of flat tensors: one bias of width n per matrix,
+four h-vectors per block (two norm layers), and four equal embedder-sized
+tensors that bring the group to the share the paper's model-configuration
+table gives for the matching scale (100% minus the Muon-routed share).  Its
+values: p ~ N(0, 0.02), g ~ 0.01 N(0, 1), first moment ~ 0.003 N(0, 1), second
+moment ~ 1.4e-5 chi^2_3 / 3 (the scale of a few averaged squared gradients).
+
 Seeds: numpy.random.SeedSequence([20818, workload, matrix, tag]).  Host draws
 use PCG64.  Device draws (large workloads) take the thin Haar factors from the
 host draw and the large Gaussian terms from a torch generator on the GPU seeded
@@ -28,7 +36,8 @@ from dataclasses import dataclass
 import numpy as np
 
 SEED_ROOT = 20818
-TAGS = {"U": 1, "V": 2, "W": 3, "M": 4, "G": 100}  # gradient of step t uses 100 + t
+TAGS = {"U": 1, "V": 2, "W": 3, "M": 4, "G": 100,  # gradient of step t uses 100 + t
+        "AP": 300, "AM": 301, "AV": 302, "AG": 400}   # aux group; its gradient of step t: 400 + t
 
 
 @dataclass(frozen=True)
@@ -70,13 +79,48 @@ WORKLOADS = (
 )
 
 
+# Muon-routed share of the trainable parameters (model-configuration table).
+MUON_ROUTED = {"dit-1.3b": 0.9869, "dit-4b": 0.9920, "dit-9b": 0.9948, "dit-15b": 0.9960}
+
+
+def aux_numels(workload: int) -> tuple:
+    """Element counts of the auxiliary AdamW group of a workload."""
+    wl = WORKLOADS[workload]
+    biases = [n for (_, n) in wl.shapes]
+    if wl.name == "tiny":
+        return tuple(biases + [256, 256, 7, 1])
+    f = MUON_ROUTED[wl.name]
+    norms = [wl.hidden] * (4 * wl.blocks)
+    total = int(round(sum(m * n for m, n in wl.shapes) * (1.0 - f) / f))
+    rest = total - sum(biases) - sum(norms)
+    q = rest // 4
+    return tuple([q, q, q, rest - 3 * q] + biases + norms)
+
+
+def host_aux(workload: int, idx: int, numel: int, *, param_dtype: str, grad_dtype: str,
+             steps=(0,)) -> dict:
+    """Seeded draws of one aux tensor: float32 arrays holding exactly the values
+    of the storage dtypes (p in param_dtype, g in grad_dtype, m and v fp32)."""
+    def rng(tag, t=0):
+        return host_rng(workload, idx, tag, t)
+
+    out = {"p": to_dtype_values(0.02 * rng("AP").standard_normal(numel, dtype=np.float32),
+                                param_dtype).astype(np.float32),
+           "m": 0.003 * rng("AM").standard_normal(numel, dtype=np.float32),
+           "v": (1.4e-5 / 3.0) * 2.0 * rng("AV").standard_gamma(1.5, numel, dtype=np.float32)}
+    for t in steps:
+        out[f"g{t}"] = to_dtype_values(0.01 * rng("AG", t).standard_normal(numel, dtype=np.float32),
+                                       grad_dtype).astype(np.float32)
+    return out
+
+
 def rank_of(wl: Workload, m: int, n: int) -> int:
     k = min(m, n)
     return k if wl.rank_cap is None else min(k, wl.rank_cap)
 
 
 def seed_sequence(workload: int, mat: int, tag: str, step: int = 0) -> np.random.SeedSequence:
-    code = TAGS[tag] + (step if tag == "G" else 0)
+    code = TAGS[tag] + (step if tag in ("G", "AG") else 0)
     return np.random.SeedSequence([SEED_ROOT, int(workload), int(mat), int(code)])
 
 

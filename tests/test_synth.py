@@ -1,4 +1,7 @@
 """The seeded input generator: reproducibility, distributions, bf16 rounding."""
+import json
+import os
+
 import numpy as np
 import torch
 
@@ -44,3 +47,21 @@ def test_workload_element_counts():
     assert abs(counts[3] / 1e9 - 12.080) < 1e-3
     assert abs(counts[4] / 1e9 - 22.649) < 1e-3
     assert len(synth.WORKLOADS[2].shapes) == 160
+
+
+def test_aux_group_matches_paper_share_and_is_seeded():
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_constants.json")))
+    share = gold["muon_routed_fraction"]["value"]
+    for w, scale in ((1, "1.3B"), (2, "4B"), (3, "9B"), (4, "15B")):
+        wl = synth.WORKLOADS[w]
+        aux = synth.aux_numels(w)
+        me = sum(m * n for m, n in wl.shapes)
+        assert abs(me / (me + sum(aux)) - share[scale]) < 1e-6
+        assert min(aux) >= 1 and len(aux) == 4 + len(wl.shapes) + 4 * wl.blocks
+    a = synth.host_aux(2, 5, 999, param_dtype="bf16", grad_dtype="bf16", steps=(0, 1))
+    b = synth.host_aux(2, 5, 999, param_dtype="bf16", grad_dtype="bf16", steps=(0, 1))
+    for k in a:
+        assert np.array_equal(a[k], b[k])
+    assert not np.array_equal(a["g0"], a["g1"])
+    assert np.array_equal(a["p"], synth.round_to_bf16(a["p"]))
+    assert np.all(a["v"] > 0)
