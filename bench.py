@@ -51,6 +51,7 @@ def parse():
     ap.add_argument("--K", type=int, default=None, help="refresh period (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel attribution period")
+    ap.add_argument("--no-aux", action="store_true", help="skip timing the aux-group AdamW step")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the measured MFMA / HBM ceilings (libprm calibration probes)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -115,6 +116,53 @@ def make_inputs(wl_idx, wl, device):
             log(f"[bench] inputs {i + 1}/{len(wl.shapes)} ({time.time() - t0:.1f}s)")
     torch.cuda.synchronize()
     return W, M, G
+
+
+def aux_adamw(wl_idx, wl, dev, stream, steps: int = 50, warmup: int = 5):
+    """Time the fused AdamW step of the workload's auxiliary (non-matrix) group:
+    HIP events around `steps` back-to-back steps (one launch each, pointers
+    bound once), inputs resident in HBM."""
+    import torch
+    import paper_2608_20818_amd as prm
+    import synth
+
+    numels = synth.aux_numels(wl_idx)
+    dt = {"f32": prm.F32, "bf16": prm.BF16}
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16}
+    P, G, Mo, V = [], [], [], []
+    for i, n in enumerate(numels):
+        h = synth.host_aux(wl_idx, i, n, param_dtype=wl.param_dtype, grad_dtype=wl.grad_dtype)
+        P.append(torch.from_numpy(h["p"]).to(dev).to(tdt[wl.param_dtype]))
+        G.append(torch.from_numpy(h["g0"]).to(dev).to(tdt[wl.grad_dtype]))
+        Mo.append(torch.from_numpy(h["m"]).to(dev))
+        V.append(torch.from_numpy(h["v"]).to(dev))
+    cfg = prm.adamw_config_default(param_dtype=dt[wl.param_dtype], grad_dtype=dt[wl.grad_dtype])
+    opt = prm.AuxAdamW(numels, cfg, stream=stream.cuda_stream)
+    opt.bind(P, G, Mo, V)
+    t = 4  # the drawn moments stand for the state after three updates
+    for _ in range(warmup):
+        opt.step_bound(t)
+        t += 1
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(steps):
+        opt.step_bound(t)
+        t += 1
+    b.record(stream)
+    torch.cuda.synchronize()
+    opt.close()
+    ms = a.elapsed_time(b) / steps
+    pb = 2 if wl.param_dtype == "bf16" else 4
+    gb = 2 if wl.grad_dtype == "bf16" else 4
+    elems = sum(numels)
+    alg = elems * (2 * pb + gb + 16)
+    ach = alg / (ms * 1e-3) / 1e9
+    return {"tensors": len(numels), "elements": elems, "ms": ms, "steps": steps,
+            "alg_bytes": alg, "bytes_per_element": 2 * pb + gb + 16,
+            "roofline": {"kernel": "adamw", "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None, "launches": 1,
+                         "mean_launch_ms": ms, "alg_per_launch": alg}}
 
 
 def cpu_baseline(wl_idx, wl, K, cfg_vals, budget_s: float = 12.0):
@@ -294,6 +342,11 @@ def main():
         log(f"[bench] kernels: " + ", ".join(f"{k} {v['total_ms']:.2f}ms/{v['launches']}" for k, v in kernels.items() if v["launches"]))
 
     opt.close()
+    aux = None
+    if not args.no_aux and wl.name in synth.MUON_ROUTED:
+        aux = aux_adamw(args.config, wl, dev, stream)
+        log(f"[bench] aux AdamW: {aux['tensors']} tensors, {aux['elements'] / 1e6:.1f} M elements, "
+            f"{aux['ms']:.3f} ms ({aux['roofline']['achieved']:.0f} GB/s)")
     peaks = None
     if not args.no_peaks:
         # the ceilings the kernels can reach on this machine: a pure MFMA loop (it
@@ -364,6 +417,8 @@ def main():
         "rowwise_alg_gb": rw_bytes / 1e9,
         "roofline": roofline,
         "roofline_rowwise": roofline_rw,
+        "aux_adamw": aux,
+        "amortized_with_aux_ms": amort + aux["ms"] if aux else None,
         "kernels": kernels,
         "cpu_baseline": cpu,
         "paper_context": "46.9-54.3% optimizer-time reduction of PRM (K=3) vs Muon on 256 H100 with "

@@ -150,6 +150,55 @@ int prm_profile_read(prm_ctx* ctx, prm_kernel_stats* out, int32_t n);
  * context.  NULL is a no-op. */
 int prm_destroy(prm_ctx* ctx);
 
+/* ---- Auxiliary AdamW group ------------------------------------------------
+ * The paper updates every parameter that is not a 2-D hidden weight matrix
+ * (biases, normalization scales and shifts, embedders) with AdamW and
+ * decoupled weight decay (Sec. 2, Muon setup; App. "Optimizer and Training
+ * Hyperparameters": aux LR 1e-4, betas (0.9, 0.95), eps 1e-8, weight decay
+ * 0.01).  This context applies that update to a fixed list of flat tensors in
+ * one fused launch.  Per element, in fp32, for the t-th update (t >= 1):
+ *
+ *   m <- beta1*m + (1-beta1)*g          v <- beta2*v + (1-beta2)*g^2
+ *   p <- p - lr*( (m/(1-beta1^t)) / (sqrt(v/(1-beta2^t)) + eps) + wd*p )
+ *
+ * and p is rounded to its storage type (RNE).  Tensors are DEVICE pointers to
+ * contiguous arrays of numel[i] elements owned by the caller: p (param_dtype)
+ * and the moments m, v (fp32) are updated in place, g (grad_dtype) is only
+ * read; they must be 16-byte aligned and must not overlap.  Same stream and
+ * error rules as prm_step (validation before anything is enqueued; the call
+ * only enqueues, except that new pointer arrays wait for the previous call's
+ * small pointer-table upload). */
+typedef struct prm_adamw_config {
+  float lr;              /* used when prm_adamw_step gets lr < 0; >= 0 */
+  float beta1, beta2;    /* in [0, 1) */
+  float eps;             /* > 0, added to the square root */
+  float wd;              /* decoupled weight decay, >= 0 */
+  int32_t param_dtype;   /* prm_dtype of p */
+  int32_t grad_dtype;    /* prm_dtype of g */
+  int32_t reserved;
+} prm_adamw_config;
+
+typedef struct prm_adamw_ctx prm_adamw_ctx; /* opaque */
+
+/* Fill *cfg with the paper's aux-AdamW settings: lr = 1e-4, betas = (0.9,
+ * 0.95), eps = 1e-8, wd = 0.01, bf16 p and g. */
+void prm_adamw_config_default(prm_adamw_config* cfg);
+
+/* Create a context for n_tensors >= 0 flat tensors of numel[i] >= 0 elements
+ * (host array).  Allocates the chunk table (one entry per 2048 elements) and
+ * the pointer table on the current device and records `hip_stream`. */
+int prm_adamw_init(prm_adamw_ctx** out, int32_t n_tensors, const int64_t* numel,
+                   const prm_adamw_config* cfg, void* hip_stream);
+
+/* The t-th AdamW update (t >= 1: the number of updates so far, this one
+ * included) of every tensor, enqueued on the context's stream.  lr < 0 uses
+ * cfg->lr.  Pointers of empty tensors may be NULL. */
+int prm_adamw_step(prm_adamw_ctx* ctx, void* const* params, const void* const* grads,
+                   float* const* exp_avg, float* const* exp_avg_sq, int64_t t, float lr);
+
+/* Free the context (after synchronizing its stream).  NULL is a no-op. */
+int prm_adamw_destroy(prm_adamw_ctx* ctx);
+
 /* Calibration probes (not part of the optimizer step).  They measure the
  * ceilings the step's kernels are compared against, on the device current on
  * the calling thread, with the instructions the step uses; each call

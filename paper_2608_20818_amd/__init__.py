@@ -12,7 +12,8 @@ import ctypes
 import os
 
 __all__ = [
-    "PRMError", "Config", "KernelStats", "Optimizer", "load", "config_default",
+    "PRMError", "Config", "KernelStats", "Optimizer", "AdamWConfig", "AuxAdamW", "load",
+    "config_default", "adamw_config_default",
     "is_refresh", "workspace_bytes", "PRM_OK", "PRM_EINVAL", "PRM_EDTYPE", "PRM_EALIGN",
     "PRM_ENOMEM", "PRM_EHIP", "F32", "BF16", "KERNEL_CLASSES",
 ]
@@ -43,6 +44,14 @@ class Config(ctypes.Structure):
         ("grad_dtype", ctypes.c_int32), ("never_refresh", ctypes.c_int32),
         ("gamma_on_refresh", ctypes.c_int32), ("reserved", ctypes.c_int32),
         ("workspace_budget_bytes", ctypes.c_uint64),
+    ]
+
+
+class AdamWConfig(ctypes.Structure):
+    _fields_ = [
+        ("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+        ("eps", ctypes.c_float), ("wd", ctypes.c_float), ("param_dtype", ctypes.c_int32),
+        ("grad_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]
 
 
@@ -93,6 +102,15 @@ def load() -> ctypes.CDLL:
     L.prm_peak_mfma.restype = ctypes.c_int
     L.prm_peak_hbm.argtypes = [P, ctypes.c_uint64, dp, dp, dp, dp]
     L.prm_peak_hbm.restype = ctypes.c_int
+    L.prm_adamw_config_default.argtypes = [ctypes.POINTER(AdamWConfig)]
+    L.prm_adamw_config_default.restype = None
+    L.prm_adamw_init.argtypes = [ctypes.POINTER(P), ctypes.c_int32, i64p, ctypes.POINTER(AdamWConfig), P]
+    L.prm_adamw_init.restype = ctypes.c_int
+    L.prm_adamw_step.argtypes = [P, ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(P),
+                                 ctypes.POINTER(P), ctypes.c_int64, ctypes.c_float]
+    L.prm_adamw_step.restype = ctypes.c_int
+    L.prm_adamw_destroy.argtypes = [P]
+    L.prm_adamw_destroy.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -135,6 +153,8 @@ def _stream_handle(stream):
     if stream is None:
         import torch
         stream = torch.cuda.current_stream().cuda_stream
+    if hasattr(stream, "cuda_stream"):  # a torch.cuda.Stream
+        stream = stream.cuda_stream
     return ctypes.c_void_p(int(stream) if stream else 0)
 
 
@@ -220,6 +240,93 @@ class Optimizer:
     def close(self):
         if getattr(self, "_ctx", None) is not None and self._ctx.value:
             _check(load().prm_destroy(self._ctx))
+        self._ctx = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def adamw_config_default(**overrides) -> AdamWConfig:
+    """The paper's aux-AdamW settings (see prm.h), with keyword overrides."""
+    c = AdamWConfig()
+    load().prm_adamw_config_default(ctypes.byref(c))
+    for k, v in overrides.items():
+        setattr(c, k, v)
+    return c
+
+
+class AuxAdamW:
+    """One fused-AdamW context over a fixed list of flat tensors (the non-matrix
+    parameters).  ``step`` takes lists of device tensors (or raw pointers):
+    parameters in ``cfg.param_dtype``, gradients in ``cfg.grad_dtype``, fp32
+    first and second moments, each contiguous with the element count given at
+    construction."""
+
+    def __init__(self, numels, cfg: AdamWConfig | None = None, stream=None):
+        self.numels = [int(n) for n in numels]
+        self.cfg = cfg if cfg is not None else adamw_config_default()
+        h = _stream_handle(stream)
+        self.stream = h.value or 0
+        n = len(self.numels)
+        arr = (ctypes.c_int64 * max(n, 1))(*self.numels)
+        ctx = ctypes.c_void_p()
+        _check(load().prm_adamw_init(ctypes.byref(ctx), n, arr, ctypes.byref(self.cfg), h))
+        self._ctx = ctx
+
+    def _check_tensors(self, xs, dtype_name, what):
+        if len(xs) != len(self.numels):
+            raise ValueError(f"{what}: expected {len(self.numels)} entries, got {len(xs)}")
+        for i, (x, k) in enumerate(zip(xs, self.numels)):
+            if x is None or isinstance(x, int):
+                continue
+            if x.numel() != k or not x.is_contiguous() or str(x.dtype) != f"torch.{dtype_name}":
+                raise ValueError(f"{what}[{i}]: need contiguous {dtype_name} with {k} elements, got "
+                                 f"{x.dtype} {x.numel()} contiguous={x.is_contiguous()}")
+
+    def step(self, params, grads, exp_avg, exp_avg_sq, t: int, lr: float = -1.0):
+        """Enqueue the t-th AdamW update (t >= 1, this one included)."""
+        self._check_tensors(params, _DT[self.cfg.param_dtype], "params")
+        self._check_tensors(grads, _DT[self.cfg.grad_dtype], "grads")
+        self._check_tensors(exp_avg, "float32", "exp_avg")
+        self._check_tensors(exp_avg_sq, "float32", "exp_avg_sq")
+        n = len(self.numels)
+        arr = ctypes.c_void_p * max(n, 1)
+
+        def ptrs(xs):
+            return arr(*[0 if x is None else _ptr(x) for x in xs])
+        _check(load().prm_adamw_step(self._ctx, ptrs(params), ptrs(grads), ptrs(exp_avg),
+                                     ptrs(exp_avg_sq), int(t), float(lr)))
+
+    def bind(self, params, grads, exp_avg, exp_avg_sq):
+        """Validate and keep a fixed set of tensors so that ``step_bound`` costs
+        one C call (for loops over persistent tensors)."""
+        self._check_tensors(params, _DT[self.cfg.param_dtype], "params")
+        self._check_tensors(grads, _DT[self.cfg.grad_dtype], "grads")
+        self._check_tensors(exp_avg, "float32", "exp_avg")
+        self._check_tensors(exp_avg_sq, "float32", "exp_avg_sq")
+        arr = ctypes.c_void_p * max(len(self.numels), 1)
+
+        def ptrs(xs):
+            return arr(*[0 if x is None else _ptr(x) for x in xs])
+        self._keep = (list(params), list(grads), list(exp_avg), list(exp_avg_sq))
+        self._bound = (ptrs(params), ptrs(grads), ptrs(exp_avg), ptrs(exp_avg_sq))
+
+    def step_bound(self, t: int, lr: float = -1.0):
+        """``step`` on the tensors given to ``bind``."""
+        _check(load().prm_adamw_step(self._ctx, *self._bound, int(t), float(lr)))
+
+    def close(self):
+        if getattr(self, "_ctx", None) is not None and self._ctx.value:
+            _check(load().prm_adamw_destroy(self._ctx))
         self._ctx = None
 
     def __enter__(self):

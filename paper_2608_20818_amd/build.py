@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libprm.so")
-SOURCES = ("prm_api.hip", "rowwise.hip", "ns5.hip", "probe.hip")
+SOURCES = ("prm_api.hip", "rowwise.hip", "ns5.hip", "probe.hip", "adamw.hip")
 ARCH = "gfx950"
 
 FLAGS = [

@@ -580,6 +580,41 @@ int do_step(prm_ctx* c, void* const* params, const void* const* grads, float* co
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// auxiliary AdamW group
+// ---------------------------------------------------------------------------
+struct prm_adamw_ctx {
+  prm_adamw_config cfg;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  std::vector<int64_t> numel;
+  std::vector<AuxDesc> desc;
+  AuxDesc* d_desc = nullptr;
+  AuxDesc* h_desc = nullptr;  // pinned staging of the pointer table
+  AuxChunk* d_chunks = nullptr;
+  int32_t nchunks = 0;
+  hipEvent_t upload_done = nullptr;
+  bool uploaded = false;
+};
+
+namespace {
+
+int check_adamw_config(const prm_adamw_config* c) {
+  if (!c) return fail(PRM_EINVAL, "cfg is NULL");
+  if (!(c->lr >= 0.f) || !std::isfinite(c->lr)) return fail(PRM_EINVAL, "lr must be finite and >= 0");
+  if (!(c->beta1 >= 0.f && c->beta1 < 1.f)) return fail(PRM_EINVAL, "beta1 must be in [0,1)");
+  if (!(c->beta2 >= 0.f && c->beta2 < 1.f)) return fail(PRM_EINVAL, "beta2 must be in [0,1)");
+  if (!(c->eps > 0.f) || !std::isfinite(c->eps)) return fail(PRM_EINVAL, "eps must be finite and > 0");
+  if (!(c->wd >= 0.f) || !std::isfinite(c->wd)) return fail(PRM_EINVAL, "wd must be finite and >= 0");
+  if (c->param_dtype != PRM_F32 && c->param_dtype != PRM_BF16)
+    return fail(PRM_EDTYPE, "unsupported param_dtype %d", c->param_dtype);
+  if (c->grad_dtype != PRM_F32 && c->grad_dtype != PRM_BF16)
+    return fail(PRM_EDTYPE, "unsupported grad_dtype %d", c->grad_dtype);
+  return PRM_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 void prm_config_default(prm_config* cfg) {
@@ -745,6 +780,129 @@ int prm_destroy(prm_ctx* c) {
   if (c->d_items) (void)hipFree(c->d_items);
   if (c->upload_done) (void)hipEventDestroy(c->upload_done);
   for (auto e : c->pool) (void)hipEventDestroy(e);
+  delete c;
+  return rc;
+}
+
+void prm_adamw_config_default(prm_adamw_config* cfg) {
+  if (!cfg) return;
+  std::memset(cfg, 0, sizeof(*cfg));
+  cfg->lr = 1e-4f;
+  cfg->beta1 = 0.9f;
+  cfg->beta2 = 0.95f;
+  cfg->eps = 1e-8f;
+  cfg->wd = 0.01f;
+  cfg->param_dtype = PRM_BF16;
+  cfg->grad_dtype = PRM_BF16;
+}
+
+int prm_adamw_init(prm_adamw_ctx** out, int32_t n_tensors, const int64_t* numel,
+                   const prm_adamw_config* cfg, void* hip_stream) {
+  if (!out) return fail(PRM_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = check_adamw_config(cfg);
+  if (rc) return rc;
+  if (n_tensors < 0) return fail(PRM_EINVAL, "n_tensors must be >= 0");
+  if (n_tensors > 0 && !numel) return fail(PRM_EINVAL, "numel is NULL");
+  std::vector<AuxChunk> chunks;
+  for (int32_t i = 0; i < n_tensors; ++i) {
+    if (numel[i] < 0 || numel[i] > (int64_t(1) << 40))
+      return fail(PRM_EINVAL, "tensor %d has invalid size %lld", i, (long long)numel[i]);
+    for (int64_t e = 0; e < numel[i]; e += kAdamwChunk) chunks.push_back(AuxChunk{e, i, 0});
+    if (chunks.size() > (size_t)INT32_MAX) return fail(PRM_EINVAL, "aux group too large for one launch");
+  }
+  prm_adamw_ctx* c = new prm_adamw_ctx();
+  c->cfg = *cfg;
+  c->stream = (hipStream_t)hip_stream;
+  c->numel.assign(numel, numel + n_tensors);
+  c->desc.assign(n_tensors, AuxDesc{});
+  for (int32_t i = 0; i < n_tensors; ++i) c->desc[i].n = numel[i];
+  c->nchunks = (int32_t)chunks.size();
+  hipError_t e = hipGetDevice(&c->device);
+  const size_t nd = std::max<size_t>(1, (size_t)n_tensors);
+  if (e == hipSuccess) e = hipMalloc((void**)&c->d_desc, sizeof(AuxDesc) * nd);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&c->h_desc, sizeof(AuxDesc) * nd, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->upload_done, hipEventDisableTiming);
+  if (e == hipSuccess && !chunks.empty()) {
+    e = hipMalloc((void**)&c->d_chunks, sizeof(AuxChunk) * chunks.size());
+    if (e == hipSuccess)
+      e = hipMemcpy(c->d_chunks, chunks.data(), sizeof(AuxChunk) * chunks.size(), hipMemcpyHostToDevice);
+  }
+  if (e != hipSuccess) {
+    rc = fail(e == hipErrorOutOfMemory ? PRM_ENOMEM : PRM_EHIP, "prm_adamw_init: %s", hipGetErrorString(e));
+    prm_adamw_destroy(c);
+    return rc;
+  }
+  *out = c;
+  return PRM_OK;
+}
+
+int prm_adamw_step(prm_adamw_ctx* c, void* const* params, const void* const* grads, float* const* exp_avg,
+                   float* const* exp_avg_sq, int64_t t, float lr) {
+  if (!c) return fail(PRM_EINVAL, "ctx is NULL");
+  if (t < 1) return fail(PRM_EINVAL, "t must be >= 1 (got %lld)", (long long)t);
+  const float eta = lr < 0.f ? c->cfg.lr : lr;
+  if (!std::isfinite(eta)) return fail(PRM_EINVAL, "lr must be finite");
+  const int n = (int)c->numel.size();
+  if (n > 0 && (!params || !grads || !exp_avg || !exp_avg_sq))
+    return fail(PRM_EINVAL, "params/grads/exp_avg/exp_avg_sq array is NULL");
+  bool same = c->uploaded;
+  for (int i = 0; i < n; ++i) {
+    if (c->numel[i] == 0) continue;
+    const void* ps[4] = {params[i], grads[i], exp_avg[i], exp_avg_sq[i]};
+    for (int k = 0; k < 4; ++k) {
+      if (!ps[k]) return fail(PRM_EINVAL, "tensor %d: NULL device pointer (argument %d)", i, k);
+      if ((uintptr_t)ps[k] % 16) return fail(PRM_EALIGN, "tensor %d: pointer %d is not 16-byte aligned", i, k);
+    }
+    const AuxDesc& d = c->desc[i];
+    same = same && d.P == params[i] && d.G == grads[i] && d.M == exp_avg[i] && d.V == exp_avg_sq[i];
+  }
+  if (c->nchunks == 0) return PRM_OK;
+  HIP_TRY(hipSetDevice(c->device));
+  if (!same) {
+    if (c->uploaded) HIP_TRY(hipEventSynchronize(c->upload_done));
+    for (int i = 0; i < n; ++i) {
+      AuxDesc& d = c->desc[i];
+      if (c->numel[i] == 0) {
+        d.P = nullptr; d.G = nullptr; d.M = nullptr; d.V = nullptr;
+        continue;
+      }
+      d.P = params[i];
+      d.G = grads[i];
+      d.M = exp_avg[i];
+      d.V = exp_avg_sq[i];
+    }
+    std::memcpy(c->h_desc, c->desc.data(), sizeof(AuxDesc) * n);
+    HIP_TRY(hipMemcpyAsync(c->d_desc, c->h_desc, sizeof(AuxDesc) * n, hipMemcpyHostToDevice, c->stream));
+    HIP_TRY(hipEventRecord(c->upload_done, c->stream));
+    c->uploaded = true;
+  }
+  const double b1 = c->cfg.beta1, b2 = c->cfg.beta2;
+  const double bc1 = 1.0 - std::pow(b1, (double)t), bc2 = 1.0 - std::pow(b2, (double)t);
+  AdamwParams a;
+  a.beta1 = (float)b1;
+  a.beta2 = (float)b2;
+  a.omb1 = (float)(1.0 - b1);
+  a.omb2 = (float)(1.0 - b2);
+  a.eps = c->cfg.eps;
+  a.decay = (float)(1.0 - (double)eta * (double)c->cfg.wd);
+  a.step_size = (float)((double)eta / bc1);
+  a.inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+  hipError_t e = launch_adamw((DType)c->cfg.param_dtype, (DType)c->cfg.grad_dtype, c->d_desc, c->d_chunks,
+                              c->nchunks, a, c->stream);
+  if (e != hipSuccess) return fail(PRM_EHIP, "adamw launch failed: %s", hipGetErrorString(e));
+  return PRM_OK;
+}
+
+int prm_adamw_destroy(prm_adamw_ctx* c) {
+  if (!c) return PRM_OK;
+  int rc = PRM_OK;
+  if (c->d_desc && hipStreamSynchronize(c->stream) != hipSuccess)
+    rc = fail(PRM_EHIP, "hipStreamSynchronize failed in prm_adamw_destroy");
+  if (c->d_desc) (void)hipFree(c->d_desc);
+  if (c->h_desc) (void)hipHostFree(c->h_desc);
+  if (c->d_chunks) (void)hipFree(c->d_chunks);
+  if (c->upload_done) (void)hipEventDestroy(c->upload_done);
   delete c;
   return rc;
 }

@@ -105,9 +105,40 @@ hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item
 
 // calibration probes (probe.hip)
 hipError_t launch_probe_mfma(int blocks, float* sink, unsigned long long* clk, int iters, hipStream_t s);
-// kind 0: read x, 1: write y, 2: copy x -> y; n16 16-byte elements
+// kind 0: read x, 1: write y, 2: copy x -> y; n16 16-byte elements; kind 3:
+// the row-wise step's traffic over n16 pieces of 4 elements (x: fp32, y: 2 x bf16)
 hipError_t launch_probe_stream(int kind, int blocks, const void* x, void* y, int64_t n16, unsigned* sink,
                                hipStream_t s);
+
+// ---- auxiliary AdamW group (adamw.hip) ------------------------------------
+// One entry per tensor of the group, in the order given to prm_adamw_init;
+// pointers are refreshed whenever the caller passes different ones.
+struct AuxDesc {
+  void* P;        // parameter (param dtype)
+  const void* G;  // gradient (grad dtype)
+  float* M;       // first moment
+  float* V;       // second moment
+  int64_t n;      // elements
+  int64_t pad;
+};
+// A block's share: kAdamwChunk consecutive elements of one tensor.
+struct AuxChunk {
+  int64_t start;
+  int32_t t;
+  int32_t pad;
+};
+// Per-launch scalars (bias corrections folded in on the host, in double).
+struct AdamwParams {
+  float beta1, beta2;
+  float omb1, omb2;      // 1 - beta1, 1 - beta2
+  float eps;
+  float decay;           // 1 - lr * wd
+  float step_size;       // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
+};
+constexpr int kAdamwChunk = 2048;  // elements per block: 256 threads x 2 pieces of 4
+hipError_t launch_adamw(DType pt, DType gt, const AuxDesc* desc, const AuxChunk* chunks, int32_t nchunks,
+                        const AdamwParams& p, hipStream_t s);
 
 // GEMM tile edge used by the NS5 kernels; rp and cp are multiples of it.
 constexpr int kNsTile = 256;

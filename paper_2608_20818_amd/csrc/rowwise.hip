@@ -145,8 +145,8 @@ __global__ __launch_bounds__(256) void rw_generic_kernel(const MatDesc* __restri
   float ss = 0.f;
   for (int64_t e = threadIdx.x; e < n; e += 256) {
     const float g = VecNT<GT>::load1(G + e);
-    float m = p.beta * M[e] + p.gcoef * g;
-    M[e] = m;
+    float m = p.beta * Vec<float>::load1(M + e) + p.gcoef * g;
+    Vec<float>::store1(M + e, m);
     const float u = p.nesterov ? g + p.beta * m : m;
     ss += u * u;
   }
@@ -155,11 +155,11 @@ __global__ __launch_bounds__(256) void rw_generic_kernel(const MatDesc* __restri
   const float kcoef = p.gamma * d.s * (1.0f / nu);
   float* Dp = d.D + row * n;
   for (int64_t e = threadIdx.x; e < n; e += 256) {
-    const float m = M[e];
+    const float m = Vec<float>::load1(M + e);
     const float u = p.nesterov ? VecNT<GT>::load1(G + e) + p.beta * m : m;
     const float dv = u * kcoef;
     VecNT<WT>::store1(W + e, VecNT<WT>::load1(W + e) * p.decay - p.lr * dv);
-    if (p.write_d) Dp[e] = dv;
+    if (p.write_d) Vec<float>::store1(Dp + e, dv);
   }
 }
 
@@ -196,7 +196,7 @@ __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __res
           VecNT<float>::load4(M + off, m[q]);
         } else {
           g[q][0] = VecNT<GT>::load1(G + off);
-          m[q][0] = M[off];
+          m[q][0] = Vec<float>::load1(M + off);
         }
       }
 #pragma unroll
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __res
         const int64_t off = (r + q) * n + col;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) m[q][k] = p.beta * m[q][k] + p.gcoef * g[q][k];
-        if constexpr (VEC == 4) VecNT<float>::store4(M + off, m[q]); else M[off] = m[q][0];
+        if constexpr (VEC == 4) VecNT<float>::store4(M + off, m[q]); else Vec<float>::store1(M + off, m[q][0]);
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
           const float u = p.nesterov ? g[q][k] + p.beta * m[q][k] : m[q][k];
@@ -220,11 +220,11 @@ __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __res
         VecNT<float>::load4(M + off, m);
       } else {
         g[0] = VecNT<GT>::load1(G + off);
-        m[0] = M[off];
+        m[0] = Vec<float>::load1(M + off);
       }
 #pragma unroll
       for (int k = 0; k < VEC; ++k) m[k] = p.beta * m[k] + p.gcoef * g[k];
-      if constexpr (VEC == 4) VecNT<float>::store4(M + off, m); else M[off] = m[0];
+      if constexpr (VEC == 4) VecNT<float>::store4(M + off, m); else Vec<float>::store1(M + off, m[0]);
 #pragma unroll
       for (int k = 0; k < VEC; ++k) {
         const float u = p.nesterov ? g[k] + p.beta * m[k] : m[k];
@@ -232,7 +232,7 @@ __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __res
       }
     }
     float* cp = d.colpart + (int64_t)it.tm * n + col;
-    if constexpr (VEC == 4) VecNT<float>::store4(cp, acc); else cp[0] = acc[0];
+    if constexpr (VEC == 4) VecNT<float>::store4(cp, acc); else Vec<float>::store1(cp, acc[0]);
   }
 }
 
@@ -246,8 +246,8 @@ __global__ __launch_bounds__(256) void rw_tall_finalize_kernel(const MatDesc* __
   const int64_t col = (int64_t)it.tn * 256 + threadIdx.x;
   if (col >= d.n) return;
   float s = 0.f;
-  for (int rb = 0; rb < d.nrb; ++rb) s += d.colpart[(int64_t)rb * d.n + col];
-  d.colinv[col] = 1.0f / fmaxf(sqrtf(s), p.eps);
+  for (int rb = 0; rb < d.nrb; ++rb) s += Vec<float>::load1(d.colpart + (int64_t)rb * d.n + col);
+  Vec<float>::store1(d.colinv + col, 1.0f / fmaxf(sqrtf(s), p.eps));
 }
 
 // Tall pass 2: D = gamma * s * U / nu_col and the parameter write.
@@ -270,7 +270,7 @@ __global__ __launch_bounds__(256) void rw_tall_apply_kernel(const MatDesc* __res
   float kc[VEC];
   const float gs = p.gamma * d.s;
 #pragma unroll
-  for (int k = 0; k < VEC; ++k) kc[k] = gs * d.colinv[col + k];
+  for (int k = 0; k < VEC; ++k) kc[k] = gs * Vec<float>::load1(d.colinv + col + k);
   constexpr int UNR = 8;
   for (int64_t r = r0; r < r1; r += UNR) {
     float m[UNR][VEC], w[UNR][VEC], g[UNR][VEC];
@@ -283,7 +283,7 @@ __global__ __launch_bounds__(256) void rw_tall_apply_kernel(const MatDesc* __res
           VecNT<WT>::load4(W + off, w[q]);
           if (p.nesterov) VecNT<GT>::load4(G + off, g[q]);
         } else {
-          m[q][0] = M[off];
+          m[q][0] = Vec<float>::load1(M + off);
           w[q][0] = VecNT<WT>::load1(W + off);
           if (p.nesterov) g[q][0] = VecNT<GT>::load1(G + off);
         }
@@ -305,7 +305,7 @@ __global__ __launch_bounds__(256) void rw_tall_apply_kernel(const MatDesc* __res
           if (p.write_d) VecNT<float>::store4(d.D + off, dv);
         } else {
           VecNT<WT>::store1(W + off, w[q][0]);
-          if (p.write_d) d.D[off] = dv[0];
+          if (p.write_d) Vec<float>::store1(d.D + off, dv[0]);
         }
       }
     }

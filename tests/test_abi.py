@@ -5,6 +5,7 @@ import os
 import re
 import subprocess
 
+import numpy as np
 import pytest
 
 import paper_2608_20818_amd as prm
@@ -145,3 +146,42 @@ def test_calibration_probes_validate_before_touching_the_device():
     assert L.prm_peak_hbm(None, 1 << 30, ctypes.byref(d), ctypes.byref(d), ctypes.byref(d), None) == prm.PRM_EINVAL
     assert L.prm_peak_hbm(None, 1000, ctypes.byref(d), ctypes.byref(d), ctypes.byref(d), ctypes.byref(d)) == prm.PRM_EINVAL
     assert L.prm_last_error().decode() != ""
+
+
+def test_adamw_config_layout_and_defaults_are_paper_values():
+    # prm_adamw_config: 5 floats, 3 int32
+    assert ctypes.sizeof(prm.AdamWConfig) == 32
+    c = prm.adamw_config_default()
+    gold = po.AdamWConfig()
+    for got, want in ((c.lr, gold.lr), (c.beta1, gold.beta1), (c.beta2, gold.beta2), (c.eps, gold.eps),
+                      (c.wd, gold.wd)):
+        assert got == np.float32(want)
+    assert c.param_dtype == prm.BF16 and c.grad_dtype == prm.BF16
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("lr", -1.0, prm.PRM_EINVAL), ("beta1", 1.0, prm.PRM_EINVAL), ("beta2", -0.1, prm.PRM_EINVAL),
+    ("eps", 0.0, prm.PRM_EINVAL), ("wd", float("nan"), prm.PRM_EINVAL),
+    ("param_dtype", 3, prm.PRM_EDTYPE), ("grad_dtype", 9, prm.PRM_EDTYPE),
+])
+def test_adamw_init_validates_before_touching_the_device(field, value, code):
+    cfg = prm.adamw_config_default(**{field: value})
+    L = prm.load()
+    numel = (ctypes.c_int64 * 2)(10, 4096)
+    ctx = ctypes.c_void_p(123)
+    assert L.prm_adamw_init(ctypes.byref(ctx), 2, numel, ctypes.byref(cfg), None) == code
+    assert ctx.value is None
+    assert L.prm_last_error().decode() != ""
+
+
+def test_adamw_bad_sizes_and_null_context():
+    L = prm.load()
+    cfg = prm.adamw_config_default()
+    ctx = ctypes.c_void_p()
+    assert L.prm_adamw_init(ctypes.byref(ctx), -1, None, ctypes.byref(cfg), None) == prm.PRM_EINVAL
+    assert L.prm_adamw_init(ctypes.byref(ctx), 2, None, ctypes.byref(cfg), None) == prm.PRM_EINVAL
+    bad = (ctypes.c_int64 * 2)(5, -1)
+    assert L.prm_adamw_init(ctypes.byref(ctx), 2, bad, ctypes.byref(cfg), None) == prm.PRM_EINVAL
+    assert L.prm_adamw_init(None, 0, None, ctypes.byref(cfg), None) == prm.PRM_EINVAL
+    assert L.prm_adamw_step(None, None, None, None, None, 1, -1.0) == prm.PRM_EINVAL
+    assert L.prm_adamw_destroy(None) == prm.PRM_OK
