@@ -277,7 +277,7 @@ void build_lists(Plan& P, const prm_config* cfg) {
   for (int i = 0; i < P.n; ++i) {
     if (!P.tall[i]) continue;
     const int vec = (P.nn[i] % 4 == 0) ? 4 : 1;
-    const int64_t slabs = (P.nn[i] + 256 * vec - 1) / (256 * vec);
+    const int64_t slabs = (P.nn[i] + 255) / 256;  // 256-column tiles
     auto& L = vec == 4 ? P.tall_items4 : P.tall_items1;
     for (int32_t rb = 0; rb < P.nrb[i]; ++rb)
       for (int32_t sb = 0; sb < slabs; ++sb) L.push_back(Item{i, rb, sb, 0});

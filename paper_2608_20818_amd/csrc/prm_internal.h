@@ -144,7 +144,7 @@ hipError_t launch_adamw(DType pt, DType gt, const AuxDesc* desc, const AuxChunk*
 constexpr int kNsTile = 256;
 // Prologue tile edge.
 constexpr int kPrologueTile = 64;
-// Row block of the tall statistics pass.
-constexpr int kTallRows = 128;
+// Row block of the tall passes (rows of one 256-column tile; 8 per wave).
+constexpr int kTallRows = 32;
 
 }  // namespace prm

@@ -164,76 +164,95 @@ __global__ __launch_bounds__(256) void rw_generic_kernel(const MatDesc* __restri
 }
 
 // ---------------------------------------------------------------------------
-// Tall pass 1: momentum update and partial column sums of squares over a row
-// block of kTallRows rows and a slab of 256*VEC columns.
+// Tall pass 1: momentum update and partial column sums of squares.
+//
+// n % 4 == 0: one block per tile of kTallRows (32) rows x 256 columns, and
+// every thread loads its whole share once: wave w takes rows 8w .. 8w+7 of the
+// tile, lane l the 4 columns 4l .. 4l+3, so each load or store instruction
+// covers one contiguous 1 KB (fp32) or 512 B (bf16) span of a row.  Grids of
+// such one-shot blocks stream HBM ~13% faster than blocks that loop over
+// rows.  The four waves' column sums meet in LDS and wave 0 writes the
+// tile's partial (fixed order).
 // ---------------------------------------------------------------------------
-template <int VEC, DType GD>
+constexpr int kTallRowsPerWave = kTallRows / 4;
+static_assert(kTallRows % 4 == 0, "four waves share a tile's rows");
+
+template <DType GD>
 __global__ __launch_bounds__(256) void rw_tall_stats_kernel(const MatDesc* __restrict__ md,
                                                             const Item* __restrict__ items,
                                                             RwParams p) {
   using GT = typename Store<GD>::T;
+  constexpr int U = kTallRowsPerWave;
+  __shared__ float red[4][64][4];
   const Item it = items[blockIdx.x];
   const MatDesc& d = md[it.mat];
   const int64_t n = d.n;
-  const int64_t col = (int64_t)it.tn * 256 * VEC + threadIdx.x * VEC;
-  const int64_t r0 = (int64_t)it.tm * kTallRows;
-  const int64_t r1 = min(d.m, r0 + kTallRows);
-  float acc[VEC];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t col = (int64_t)it.tn * 256 + 4 * lane;
+  const int64_t r0 = (int64_t)it.tm * kTallRows + w * U;
+  const bool ok = col < n;
+  const GT* G = reinterpret_cast<const GT*>(d.G);
+  float* M = d.M;
+  float g[U][4], m[U][4];
 #pragma unroll
-  for (int k = 0; k < VEC; ++k) acc[k] = 0.f;
-  if (col < n) {
-    const GT* G = reinterpret_cast<const GT*>(d.G);
-    float* M = d.M;
-    constexpr int UNR = 8;
-    int64_t r = r0;
-    for (; r + UNR <= r1; r += UNR) {
-      float g[UNR][VEC], m[UNR][VEC];
-#pragma unroll
-      for (int q = 0; q < UNR; ++q) {
-        const int64_t off = (r + q) * n + col;
-        if constexpr (VEC == 4) {
-          VecNT<GT>::load4(G + off, g[q]);
-          VecNT<float>::load4(M + off, m[q]);
-        } else {
-          g[q][0] = VecNT<GT>::load1(G + off);
-          m[q][0] = Vec<float>::load1(M + off);
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < UNR; ++q) {
-        const int64_t off = (r + q) * n + col;
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) m[q][k] = p.beta * m[q][k] + p.gcoef * g[q][k];
-        if constexpr (VEC == 4) VecNT<float>::store4(M + off, m[q]); else Vec<float>::store1(M + off, m[q][0]);
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-          const float u = p.nesterov ? g[q][k] + p.beta * m[q][k] : m[q][k];
-          acc[k] += u * u;
-        }
-      }
+  for (int q = 0; q < U; ++q) {
+    if (ok && r0 + q < d.m) {
+      const int64_t off = (r0 + q) * n + col;
+      VecNT<GT>::load4(G + off, g[q]);
+      VecNT<float>::load4(M + off, m[q]);
     }
-    for (; r < r1; ++r) {
-      const int64_t off = r * n + col;
-      float g[VEC], m[VEC];
-      if constexpr (VEC == 4) {
-        VecNT<GT>::load4(G + off, g);
-        VecNT<float>::load4(M + off, m);
-      } else {
-        g[0] = VecNT<GT>::load1(G + off);
-        m[0] = Vec<float>::load1(M + off);
-      }
+  }
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int k = 0; k < VEC; ++k) m[k] = p.beta * m[k] + p.gcoef * g[k];
-      if constexpr (VEC == 4) VecNT<float>::store4(M + off, m); else Vec<float>::store1(M + off, m[0]);
+  for (int q = 0; q < U; ++q) {
+    if (ok && r0 + q < d.m) {
+      const int64_t off = (r0 + q) * n + col;
 #pragma unroll
-      for (int k = 0; k < VEC; ++k) {
-        const float u = p.nesterov ? g[k] + p.beta * m[k] : m[k];
+      for (int k = 0; k < 4; ++k) m[q][k] = p.beta * m[q][k] + p.gcoef * g[q][k];
+      VecNT<float>::store4(M + off, m[q]);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float u = p.nesterov ? g[q][k] + p.beta * m[q][k] : m[q][k];
         acc[k] += u * u;
       }
     }
-    float* cp = d.colpart + (int64_t)it.tm * n + col;
-    if constexpr (VEC == 4) VecNT<float>::store4(cp, acc); else Vec<float>::store1(cp, acc[0]);
   }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) red[w][lane][k] = acc[k];
+  __syncthreads();
+  if (w == 0 && ok) {
+    float s[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s[k] = ((red[0][lane][k] + red[1][lane][k]) + red[2][lane][k]) + red[3][lane][k];
+    VecNT<float>::store4(d.colpart + (int64_t)it.tm * n + col, s);
+  }
+}
+
+// n % 4 != 0: one column per thread, 256 columns and kTallRows rows per block.
+template <DType GD>
+__global__ __launch_bounds__(256) void rw_tall_stats_scalar_kernel(const MatDesc* __restrict__ md,
+                                                                   const Item* __restrict__ items,
+                                                                   RwParams p) {
+  using GT = typename Store<GD>::T;
+  const Item it = items[blockIdx.x];
+  const MatDesc& d = md[it.mat];
+  const int64_t n = d.n;
+  const int64_t col = (int64_t)it.tn * 256 + threadIdx.x;
+  if (col >= n) return;
+  const int64_t r0 = (int64_t)it.tm * kTallRows;
+  const int64_t r1 = min(d.m, r0 + kTallRows);
+  const GT* G = reinterpret_cast<const GT*>(d.G);
+  float* M = d.M;
+  float acc = 0.f;
+  for (int64_t r = r0; r < r1; ++r) {
+    const int64_t off = r * n + col;
+    const float g = VecNT<GT>::load1(G + off);
+    const float m = p.beta * Vec<float>::load1(M + off) + p.gcoef * g;
+    Vec<float>::store1(M + off, m);
+    const float u = p.nesterov ? g + p.beta * m : m;
+    acc += u * u;
+  }
+  Vec<float>::store1(d.colpart + (int64_t)it.tm * n + col, acc);
 }
 
 // Column norms of a tall matrix: fixed-order sum over row blocks, square root,
@@ -245,70 +264,98 @@ __global__ __launch_bounds__(256) void rw_tall_finalize_kernel(const MatDesc* __
   const MatDesc& d = md[it.mat];
   const int64_t col = (int64_t)it.tn * 256 + threadIdx.x;
   if (col >= d.n) return;
+  // the loads of 16 row blocks are issued together; the additions keep the
+  // row-block order
+  const float* cp = d.colpart + col;
   float s = 0.f;
-  for (int rb = 0; rb < d.nrb; ++rb) s += Vec<float>::load1(d.colpart + (int64_t)rb * d.n + col);
+  int rb = 0;
+  for (; rb + 16 <= d.nrb; rb += 16) {
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = Vec<float>::load1(cp + (int64_t)(rb + k) * d.n);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) s += v[k];
+  }
+  for (; rb < d.nrb; ++rb) s += Vec<float>::load1(cp + (int64_t)rb * d.n);
   Vec<float>::store1(d.colinv + col, 1.0f / fmaxf(sqrtf(s), p.eps));
 }
 
-// Tall pass 2: D = gamma * s * U / nu_col and the parameter write.
-template <int VEC, DType WD, DType GD>
+// Tall pass 2: D = gamma * s * U / nu_col and the parameter write, on the
+// same one-shot tiles as pass 1 (n % 4 == 0).
+template <DType WD, DType GD, bool NEST>
 __global__ __launch_bounds__(256) void rw_tall_apply_kernel(const MatDesc* __restrict__ md,
                                                             const Item* __restrict__ items,
                                                             RwParams p) {
   using WT = typename Store<WD>::T;
   using GT = typename Store<GD>::T;
+  constexpr int U = kTallRowsPerWave;
   const Item it = items[blockIdx.x];
   const MatDesc& d = md[it.mat];
   const int64_t n = d.n;
-  const int64_t col = (int64_t)it.tn * 256 * VEC + threadIdx.x * VEC;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t col = (int64_t)it.tn * 256 + 4 * lane;
+  if (col >= n) return;
+  const int64_t r0 = (int64_t)it.tm * kTallRows + w * U;
+  const GT* G = reinterpret_cast<const GT*>(d.G);
+  const float* M = d.M;
+  WT* W = reinterpret_cast<WT*>(d.W);
+  float m[U][4], wv[U][4], g[NEST ? U : 1][4];
+#pragma unroll
+  for (int q = 0; q < U; ++q) {
+    if (r0 + q < d.m) {
+      const int64_t off = (r0 + q) * n + col;
+      VecNT<float>::load4(M + off, m[q]);
+      VecNT<WT>::load4(W + off, wv[q]);
+      if constexpr (NEST) VecNT<GT>::load4(G + off, g[q]);
+    }
+  }
+  float kc[4];
+  Vec<float>::load4(d.colinv + col, kc);  // shared by every tile of these columns: cached
+  const float gs = p.gamma * d.s;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) kc[k] *= gs;
+#pragma unroll
+  for (int q = 0; q < U; ++q) {
+    if (r0 + q < d.m) {
+      const int64_t off = (r0 + q) * n + col;
+      float dv[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        float u = m[q][k];
+        if constexpr (NEST) u = g[q][k] + p.beta * m[q][k];
+        dv[k] = u * kc[k];
+        wv[q][k] = wv[q][k] * p.decay - p.lr * dv[k];
+      }
+      VecNT<WT>::store4(W + off, wv[q]);
+      if (p.write_d) VecNT<float>::store4(d.D + off, dv);
+    }
+  }
+}
+
+// n % 4 != 0: one column per thread.
+template <DType WD, DType GD>
+__global__ __launch_bounds__(256) void rw_tall_apply_scalar_kernel(const MatDesc* __restrict__ md,
+                                                                   const Item* __restrict__ items,
+                                                                   RwParams p) {
+  using WT = typename Store<WD>::T;
+  using GT = typename Store<GD>::T;
+  const Item it = items[blockIdx.x];
+  const MatDesc& d = md[it.mat];
+  const int64_t n = d.n;
+  const int64_t col = (int64_t)it.tn * 256 + threadIdx.x;
   if (col >= n) return;
   const int64_t r0 = (int64_t)it.tm * kTallRows;
   const int64_t r1 = min(d.m, r0 + kTallRows);
   const GT* G = reinterpret_cast<const GT*>(d.G);
-  const float* M = d.M;
   WT* W = reinterpret_cast<WT*>(d.W);
-  float kc[VEC];
-  const float gs = p.gamma * d.s;
-#pragma unroll
-  for (int k = 0; k < VEC; ++k) kc[k] = gs * Vec<float>::load1(d.colinv + col + k);
-  constexpr int UNR = 8;
-  for (int64_t r = r0; r < r1; r += UNR) {
-    float m[UNR][VEC], w[UNR][VEC], g[UNR][VEC];
-#pragma unroll
-    for (int q = 0; q < UNR; ++q) {
-      if (r + q < r1) {
-        const int64_t off = (r + q) * n + col;
-        if constexpr (VEC == 4) {
-          VecNT<float>::load4(M + off, m[q]);
-          VecNT<WT>::load4(W + off, w[q]);
-          if (p.nesterov) VecNT<GT>::load4(G + off, g[q]);
-        } else {
-          m[q][0] = Vec<float>::load1(M + off);
-          w[q][0] = VecNT<WT>::load1(W + off);
-          if (p.nesterov) g[q][0] = VecNT<GT>::load1(G + off);
-        }
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < UNR; ++q) {
-      if (r + q < r1) {
-        const int64_t off = (r + q) * n + col;
-        float dv[VEC];
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-          const float u = p.nesterov ? g[q][k] + p.beta * m[q][k] : m[q][k];
-          dv[k] = u * kc[k];
-          w[q][k] = w[q][k] * p.decay - p.lr * dv[k];
-        }
-        if constexpr (VEC == 4) {
-          VecNT<WT>::store4(W + off, w[q]);
-          if (p.write_d) VecNT<float>::store4(d.D + off, dv);
-        } else {
-          VecNT<WT>::store1(W + off, w[q][0]);
-          if (p.write_d) Vec<float>::store1(d.D + off, dv[0]);
-        }
-      }
-    }
+  const float kc = p.gamma * d.s * Vec<float>::load1(d.colinv + col);
+  for (int64_t r = r0; r < r1; ++r) {
+    const int64_t off = r * n + col;
+    const float m = Vec<float>::load1(d.M + off);
+    const float u = p.nesterov ? VecNT<GT>::load1(G + off) + p.beta * m : m;
+    const float dv = u * kc;
+    VecNT<WT>::store1(W + off, VecNT<WT>::load1(W + off) * p.decay - p.lr * dv);
+    if (p.write_d) Vec<float>::store1(d.D + off, dv);
   }
 }
 
@@ -372,11 +419,11 @@ hipError_t launch_rw_tall_stats(int vec, DType gt, const MatDesc* md, const Item
   if (nitems <= 0) return hipSuccess;
   dim3 g(nitems), b(256);
   if (vec == 4) {
-    if (gt == BF16) rw_tall_stats_kernel<4, BF16><<<g, b, 0, s>>>(md, items, p);
-    else rw_tall_stats_kernel<4, F32><<<g, b, 0, s>>>(md, items, p);
+    if (gt == BF16) rw_tall_stats_kernel<BF16><<<g, b, 0, s>>>(md, items, p);
+    else rw_tall_stats_kernel<F32><<<g, b, 0, s>>>(md, items, p);
   } else {
-    if (gt == BF16) rw_tall_stats_kernel<1, BF16><<<g, b, 0, s>>>(md, items, p);
-    else rw_tall_stats_kernel<1, F32><<<g, b, 0, s>>>(md, items, p);
+    if (gt == BF16) rw_tall_stats_scalar_kernel<BF16><<<g, b, 0, s>>>(md, items, p);
+    else rw_tall_stats_scalar_kernel<F32><<<g, b, 0, s>>>(md, items, p);
   }
   return hipGetLastError();
 }
@@ -388,14 +435,14 @@ hipError_t launch_rw_tall_finalize(const MatDesc* md, const Item* items, int32_t
   return hipGetLastError();
 }
 
-template <int VEC>
-static hipError_t tall_apply_vec(DType wt, DType gt, const MatDesc* md, const Item* items,
-                                 int32_t nitems, const RwParams& p, hipStream_t s) {
+template <bool NEST>
+static hipError_t tall_apply_tiles(DType wt, DType gt, const MatDesc* md, const Item* items,
+                                   int32_t nitems, const RwParams& p, hipStream_t s) {
   dim3 g(nitems), b(256);
-  if (wt == BF16 && gt == BF16) rw_tall_apply_kernel<VEC, BF16, BF16><<<g, b, 0, s>>>(md, items, p);
-  else if (wt == BF16) rw_tall_apply_kernel<VEC, BF16, F32><<<g, b, 0, s>>>(md, items, p);
-  else if (gt == BF16) rw_tall_apply_kernel<VEC, F32, BF16><<<g, b, 0, s>>>(md, items, p);
-  else rw_tall_apply_kernel<VEC, F32, F32><<<g, b, 0, s>>>(md, items, p);
+  if (wt == BF16 && gt == BF16) rw_tall_apply_kernel<BF16, BF16, NEST><<<g, b, 0, s>>>(md, items, p);
+  else if (wt == BF16) rw_tall_apply_kernel<BF16, F32, NEST><<<g, b, 0, s>>>(md, items, p);
+  else if (gt == BF16) rw_tall_apply_kernel<F32, BF16, NEST><<<g, b, 0, s>>>(md, items, p);
+  else rw_tall_apply_kernel<F32, F32, NEST><<<g, b, 0, s>>>(md, items, p);
   return hipGetLastError();
 }
 
@@ -403,8 +450,15 @@ hipError_t launch_rw_tall_apply(int vec, DType wt, DType gt, const MatDesc* md,
                                 const Item* items, int32_t nitems, const RwParams& p,
                                 hipStream_t s) {
   if (nitems <= 0) return hipSuccess;
-  return vec == 4 ? tall_apply_vec<4>(wt, gt, md, items, nitems, p, s)
-                  : tall_apply_vec<1>(wt, gt, md, items, nitems, p, s);
+  if (vec == 4)
+    return p.nesterov ? tall_apply_tiles<true>(wt, gt, md, items, nitems, p, s)
+                      : tall_apply_tiles<false>(wt, gt, md, items, nitems, p, s);
+  dim3 g(nitems), b(256);
+  if (wt == BF16 && gt == BF16) rw_tall_apply_scalar_kernel<BF16, BF16><<<g, b, 0, s>>>(md, items, p);
+  else if (wt == BF16) rw_tall_apply_scalar_kernel<BF16, F32><<<g, b, 0, s>>>(md, items, p);
+  else if (gt == BF16) rw_tall_apply_scalar_kernel<F32, BF16><<<g, b, 0, s>>>(md, items, p);
+  else rw_tall_apply_scalar_kernel<F32, F32><<<g, b, 0, s>>>(md, items, p);
+  return hipGetLastError();
 }
 
 }  // namespace prm
