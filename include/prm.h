@@ -110,7 +110,8 @@ int prm_step(prm_ctx* ctx, void* const* params, const void* const* grads,
              float* const* momentum, int64_t step, float lr, int32_t* did_refresh);
 
 /* prm_step that also writes D = s(W) * O^{-1}(D~) (fp32, m x n, row-major,
- * device) for every matrix into direction_out[i].  Parity checking only. */
+ * device) into direction_out[i] for every matrix whose entry is not NULL
+ * (NULL: that matrix's direction is not written).  Parity checking only. */
 int prm_step_debug(prm_ctx* ctx, void* const* params, const void* const* grads,
                    float* const* momentum, int64_t step, float lr, int32_t* did_refresh,
                    float* const* direction_out);

@@ -202,14 +202,15 @@ class Optimizer:
         if len(xs) != len(self.shapes):
             raise ValueError(f"{what}: expected {len(self.shapes)} entries, got {len(xs)}")
         for i, (x, s) in enumerate(zip(xs, self.shapes)):
-            if isinstance(x, int):
+            if x is None or isinstance(x, int):
                 continue
             if tuple(x.shape) != s or not x.is_contiguous() or str(x.dtype) != f"torch.{dtype_name}":
                 raise ValueError(f"{what}[{i}]: need contiguous {dtype_name} {s}, got "
                                  f"{x.dtype} {tuple(x.shape)} contiguous={x.is_contiguous()}")
 
     def step(self, params, grads, momenta, step: int, lr: float = -1.0, directions=None) -> int:
-        """Enqueue optimizer step ``step``; returns rho_t (1 = NS5 refresh)."""
+        """Enqueue optimizer step ``step``; returns rho_t (1 = NS5 refresh).
+        ``directions`` (debug): fp32 tensors receiving D, None to skip a matrix."""
         self._check_tensors(params, _DT[self.cfg.param_dtype], "params")
         self._check_tensors(grads, _DT[self.cfg.grad_dtype], "grads")
         self._check_tensors(momenta, "float32", "momenta")
@@ -224,7 +225,7 @@ class Optimizer:
             _check(L.prm_step(self._ctx, P, G, M, int(step), float(lr), ctypes.byref(rho)))
         else:
             self._check_tensors(directions, "float32", "directions")
-            D = arr(*[_ptr(x) for x in directions])
+            D = arr(*[0 if x is None else _ptr(x) for x in directions])
             _check(L.prm_step_debug(self._ctx, P, G, M, int(step), float(lr), ctypes.byref(rho), D))
         return rho.value
 

@@ -553,7 +553,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     const int64_t n = d.n;
     const float dc = d.s * p.dscale;
     WT* W = reinterpret_cast<WT*>(d.W) + wr * n;
-    float* Dp = d.D + wr * n;
+    float* const Dp = (p.write_d && d.D) ? d.D + wr * n : nullptr;
     float dv[8];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -566,13 +566,13 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
 #pragma unroll
       for (int q = 0; q < 8; ++q) w8[q] = w8[q] * p.decay - p.lr * dv[q];
       Vec<WT>::store8(W + wc, w8);
-      if (p.write_d) Vec<float>::store8(Dp + wc, dv);
+      if (Dp) Vec<float>::store8(Dp + wc, dv);
     } else {
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         if (wc + q < n) {
           Vec<WT>::store1(W + wc + q, Vec<WT>::load1(W + wc + q) * p.decay - p.lr * dv[q]);
-          if (p.write_d) Dp[wc + q] = dv[q];
+          if (Dp) Vec<float>::store1(Dp + wc + q, dv[q]);
         }
       }
     }

@@ -565,6 +565,7 @@ int do_step(prm_ctx* c, void* const* params, const void* const* grads, float* co
   for (int i = 0; i < n; ++i) {
     const void* ps[4] = {params[i], grads[i], momentum[i], debug ? (const void*)dirs[i] : nullptr};
     for (int k = 0; k < (debug ? 4 : 3); ++k) {
+      if (!ps[k] && k == 3) continue;  // direction not wanted for this matrix
       if (!ps[k]) return fail(PRM_EINVAL, "matrix %d: NULL device pointer (argument %d)", i, k);
       if ((uintptr_t)ps[k] % 16) return fail(PRM_EALIGN, "matrix %d: pointer %d is not 16-byte aligned", i, k);
     }

@@ -105,7 +105,7 @@ __global__ __launch_bounds__(NT) void rw_wide_kernel(const MatDesc* __restrict__
   ss = row_sum<NT, TPR>(ss, red);
   const float nu = fmaxf(sqrtf(ss), p.eps);
   const float kcoef = p.gamma * d.s * (1.0f / nu);
-  float* Dp = d.D + row * n;
+  float* const Dp = (p.write_d && d.D) ? d.D + row * n : nullptr;
 #pragma unroll
   for (int it = 0; it < NCH; ++it) {
     if (ok[it]) {
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(NT) void rw_wide_kernel(const MatDesc* __restrict__
         w[it][k] = w[it][k] * p.decay - p.lr * dv[k];
       }
       VecNT<WT>::store8(W + e, w[it]);
-      if (p.write_d) VecNT<float>::store8(Dp + e, dv);
+      if (Dp) VecNT<float>::store8(Dp + e, dv);
     }
   }
 }
@@ -153,13 +153,13 @@ __global__ __launch_bounds__(256) void rw_generic_kernel(const MatDesc* __restri
   ss = block_sum<256>(ss, red);
   const float nu = fmaxf(sqrtf(ss), p.eps);
   const float kcoef = p.gamma * d.s * (1.0f / nu);
-  float* Dp = d.D + row * n;
+  float* const Dp = (p.write_d && d.D) ? d.D + row * n : nullptr;
   for (int64_t e = threadIdx.x; e < n; e += 256) {
     const float m = Vec<float>::load1(M + e);
     const float u = p.nesterov ? VecNT<GT>::load1(G + e) + p.beta * m : m;
     const float dv = u * kcoef;
     VecNT<WT>::store1(W + e, VecNT<WT>::load1(W + e) * p.decay - p.lr * dv);
-    if (p.write_d) Vec<float>::store1(Dp + e, dv);
+    if (Dp) Vec<float>::store1(Dp + e, dv);
   }
 }
 
@@ -327,7 +327,7 @@ __global__ __launch_bounds__(256) void rw_tall_apply_kernel(const MatDesc* __res
         wv[q][k] = wv[q][k] * p.decay - p.lr * dv[k];
       }
       VecNT<WT>::store4(W + off, wv[q]);
-      if (p.write_d) VecNT<float>::store4(d.D + off, dv);
+      if (p.write_d && d.D) VecNT<float>::store4(d.D + off, dv);
     }
   }
 }
@@ -355,7 +355,7 @@ __global__ __launch_bounds__(256) void rw_tall_apply_scalar_kernel(const MatDesc
     const float u = p.nesterov ? VecNT<GT>::load1(G + off) + p.beta * m : m;
     const float dv = u * kc;
     VecNT<WT>::store1(W + off, VecNT<WT>::load1(W + off) * p.decay - p.lr * dv);
-    if (p.write_d) Vec<float>::store1(d.D + off, dv);
+    if (p.write_d && d.D) Vec<float>::store1(d.D + off, dv);
   }
 }
 

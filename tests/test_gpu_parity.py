@@ -239,3 +239,30 @@ def test_misaligned_pointer_rejected_without_side_effects():
         assert e.value.code == prm.PRM_EINVAL
     torch.cuda.synchronize()
     assert torch.equal(M, torch.ones_like(M))
+
+
+@pytest.mark.parametrize("t", [0, 1])
+def test_debug_step_with_some_directions_skipped(t):
+    # NULL direction entries: those matrices' D is not written; W, M and the
+    # other directions are bitwise those of a debug step with every output
+    shapes = [(64, 192), (192, 64), (130, 130), (40, 4104)]
+    cfg = prm.config_default(K=2, lr=0.02, wd=0.1, param_dtype=prm.BF16, grad_dtype=prm.BF16)
+    inputs = pc.host_inputs(shapes, cfg, 97, steps=(t,))
+    outs = []
+    for skip in (False, True):
+        W = [pc.to_device(w, cfg.param_dtype) for w, _, _ in inputs]
+        M = [pc.to_device(m, 0) for _, m, _ in inputs]
+        G = [pc.to_device(g[t], cfg.grad_dtype) for _, _, g in inputs]
+        D = [torch.full(s, 7.0, dtype=torch.float32, device="cuda") for s in shapes]
+        Dp = [None if (skip and i % 2 == 1) else x for i, x in enumerate(D)]
+        with prm.Optimizer(shapes, cfg) as opt:
+            opt.step(W, G, M, t, directions=Dp)
+            torch.cuda.synchronize()
+        outs.append((W, M, D))
+    (W0, M0, D0), (W1, M1, D1) = outs
+    for i in range(len(shapes)):
+        assert torch.equal(W0[i], W1[i]) and torch.equal(M0[i], M1[i])
+        if i % 2 == 1:
+            assert bool((D1[i] == 7.0).all()), "skipped direction was written"
+        else:
+            assert torch.equal(D0[i], D1[i])
