@@ -345,6 +345,10 @@ def main():
     aux = None
     if not args.no_aux and wl.name in synth.MUON_ROUTED:
         aux = aux_adamw(args.config, wl, dev, stream)
+        tr = counter_traffic(wl.name)
+        if tr and "adamw" in tr:
+            aux["roofline"]["traffic"] = tr["adamw"]["fetch_bytes_per_launch"] + tr["adamw"]["write_bytes_per_launch"]
+            aux["roofline"]["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
         log(f"[bench] aux AdamW: {aux['tensors']} tensors, {aux['elements'] / 1e6:.1f} M elements, "
             f"{aux['ms']:.3f} ms ({aux['roofline']['achieved']:.0f} GB/s)")
     peaks = None

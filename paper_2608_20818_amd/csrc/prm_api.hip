@@ -524,7 +524,7 @@ int refresh_step(prm_ctx* c, float lr, bool debug) {
   for (const auto& ch : P.chunks) {
     p.iter = 0;
     p.last = 0;
-    rc = timed(c, K_NS_PROLOGUE, ch.elems * (gb + 8 + 4), 0, [&] {
+    rc = timed(c, K_NS_PROLOGUE, ch.elems * (gb + 8 + 2), 0, [&] {  // G, M read; M, bf16 X^T written
       return launch_ns_prologue(gt, md, c->d_items + ch.off_prologue, (int32_t)ch.prologue.size(), p, c->stream);
     });
     if (rc) return rc;
