@@ -4,6 +4,7 @@ import ctypes
 import os
 import re
 import subprocess
+import sys
 
 import numpy as np
 import pytest
@@ -185,3 +186,11 @@ def test_adamw_bad_sizes_and_null_context():
     assert L.prm_adamw_init(None, 0, None, ctypes.byref(cfg), None) == prm.PRM_EINVAL
     assert L.prm_adamw_step(None, None, None, None, None, 1, -1.0) == prm.PRM_EINVAL
     assert L.prm_adamw_destroy(None) == prm.PRM_OK
+
+
+def test_bench_refuses_more_than_one_gpu():
+    # one GPU only: the multi-GPU path is a design note, and the bench says so
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
