@@ -100,6 +100,19 @@ def counter_traffic(workload: str):
     return t["classes"]
 
 
+def counter_mfma(workload: str):
+    """MFMA busy fraction and shader clock per GEMM kind from the committed
+    rocprofv3 SQ-counter pass, if it was taken on these kernel sources and this
+    workload; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"mfma_{workload.replace('-', '')}.json")
+    if not os.path.exists(path):
+        return None
+    t = json.load(open(path))
+    if t.get("kernel_source_sha256_16") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    return t["classes"]
+
+
 def make_inputs(wl_idx, wl, device):
     import torch
     import synth
@@ -333,6 +346,10 @@ def main():
         if rw_names:
             dom_rw = max(rw_names, key=lambda k: kernels[k]["total_ms"])
             roofline_rw = roof(dom_rw, kernels[dom_rw])
+        mf = counter_mfma(wl.name)
+        if roofline is not None and mf and roofline["kernel"] in mf:
+            roofline["mfma_busy_counters"] = mf[roofline["kernel"]]["mfma_busy"]
+            roofline["shader_clock_ghz_counters"] = mf[roofline["kernel"]]["clock_ghz"]
         traffic = counter_traffic(wl.name)
         for rf in (roofline, roofline_rw):
             if rf is not None and traffic and rf["kernel"] in traffic:
