@@ -264,19 +264,29 @@ __global__ __launch_bounds__(256) void rw_tall_finalize_kernel(const MatDesc* __
   const MatDesc& d = md[it.mat];
   const int64_t col = (int64_t)it.tn * 256 + threadIdx.x;
   if (col >= d.n) return;
-  // the loads of 16 row blocks are issued together; the additions keep the
-  // row-block order
+  // the loads of 16 row blocks are issued together and summed pairwise; the
+  // group sums are accumulated with compensation (Kahan), so the error stays
+  // at a few ulps however many row blocks a tall matrix has (fixed order)
   const float* cp = d.colpart + col;
-  float s = 0.f;
+  float s = 0.f, comp = 0.f;
+  auto add = [&](float x) {
+    const float y = x - comp;
+    const float t = s + y;
+    comp = (t - s) - y;
+    s = t;
+  };
   int rb = 0;
   for (; rb + 16 <= d.nrb; rb += 16) {
     float v[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k) v[k] = Vec<float>::load1(cp + (int64_t)(rb + k) * d.n);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) s += v[k];
+    for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+      for (int k = 0; k < w; ++k) v[k] += v[k + w];
+    add(v[0]);
   }
-  for (; rb < d.nrb; ++rb) s += Vec<float>::load1(cp + (int64_t)rb * d.n);
+  for (; rb < d.nrb; ++rb) add(Vec<float>::load1(cp + (int64_t)rb * d.n));
   Vec<float>::store1(d.colinv + col, 1.0f / fmaxf(sqrtf(s), p.eps));
 }
 

@@ -266,3 +266,15 @@ def test_debug_step_with_some_directions_skipped(t):
             assert bool((D1[i] == 7.0).all()), "skipped direction was written"
         else:
             assert torch.equal(D0[i], D1[i])
+
+
+@pytest.mark.parametrize("t", [0, 1])
+def test_long_rows_and_columns(t):
+    # extreme aspect ratios: a 4 M-element row (the two-sweep generic row-wise
+    # kernel; a Gram whose K streams 65536 stages through one tile) and a
+    # 2 M-row matrix of width 3 (scalar tall path, 65536 row tiles of partials)
+    shapes = [(2, 1 << 22), (1 << 21, 3)]
+    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=prm.BF16, grad_dtype=prm.BF16)
+    rho, res = run_one_step(shapes, cfg, t, workload_id=98)
+    assert rho == (1 if t == 0 else 0)
+    check(res, rho, cfg, shapes, cfg.lr)
