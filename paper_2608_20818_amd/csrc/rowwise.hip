@@ -142,13 +142,18 @@ __global__ __launch_bounds__(256) void rw_generic_kernel(const MatDesc* __restri
   const GT* G = reinterpret_cast<const GT*>(d.G) + row * n;
   float* M = d.M + row * n;
   WT* W = reinterpret_cast<WT*>(d.W) + row * n;
-  float ss = 0.f;
+  // a thread sums up to n / 256 squares (2^16 for the longest rows): with
+  // compensation (Kahan) the sum stays within a few ulps
+  float ss = 0.f, comp = 0.f;
   for (int64_t e = threadIdx.x; e < n; e += 256) {
     const float g = VecNT<GT>::load1(G + e);
     float m = p.beta * Vec<float>::load1(M + e) + p.gcoef * g;
     Vec<float>::store1(M + e, m);
     const float u = p.nesterov ? g + p.beta * m : m;
-    ss += u * u;
+    const float y = u * u - comp;
+    const float t = ss + y;
+    comp = (t - ss) - y;
+    ss = t;
   }
   ss = block_sum<256>(ss, red);
   const float nu = fmaxf(sqrtf(ss), p.eps);
