@@ -95,7 +95,7 @@ typedef struct prm_ctx prm_ctx; /* opaque */
 void prm_config_default(prm_config* cfg);
 
 /* Create a context for n_mats matrices of shapes rows[i] x cols[i] (host
- * arrays, each >= 1; n_mats >= 0).  Validates cfg, groups the matrices by
+ * arrays, each in [1, 2^24]; n_mats >= 0).  Validates cfg, groups the matrices by
  * oriented NS5 shape, plans and allocates the device workspace (hipMalloc on
  * the current device) and records `hip_stream` for later calls.
  * On success *out owns the workspace until prm_destroy. */

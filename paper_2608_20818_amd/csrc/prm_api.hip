@@ -100,8 +100,9 @@ int validate_cfg(const prm_config* c) {
   if (!(c->lr >= 0.f) || !std::isfinite(c->lr)) return fail(PRM_EINVAL, "lr must be finite and >= 0");
   if (!(c->wd >= 0.f) || !std::isfinite(c->wd)) return fail(PRM_EINVAL, "wd must be finite and >= 0");
   if (!(c->gamma > 0.f) || !std::isfinite(c->gamma)) return fail(PRM_EINVAL, "gamma must be > 0");
-  if (!(c->eps_rownorm > 0.f)) return fail(PRM_EINVAL, "eps_rownorm must be > 0");
-  if (!(c->eps_ns >= 0.f)) return fail(PRM_EINVAL, "eps_ns must be >= 0");
+  if (!(c->eps_rownorm > 0.f) || !std::isfinite(c->eps_rownorm))
+    return fail(PRM_EINVAL, "eps_rownorm must be finite and > 0");
+  if (!(c->eps_ns >= 0.f) || !std::isfinite(c->eps_ns)) return fail(PRM_EINVAL, "eps_ns must be finite and >= 0");
   if (!std::isfinite(c->ns_a) || !std::isfinite(c->ns_b) || !std::isfinite(c->ns_c))
     return fail(PRM_EINVAL, "NS coefficients must be finite");
   if (c->nesterov != 0 && c->nesterov != 1) return fail(PRM_EINVAL, "nesterov must be 0 or 1");
@@ -149,8 +150,6 @@ int make_plan(int32_t n_mats, const int64_t* rows, const int64_t* cols, const pr
   if (n_mats > 0 && (!rows || !cols)) return fail(PRM_EINVAL, "rows/cols is NULL");
   P = Plan();
   P.n = n_mats;
-  const int wb = cfg->param_dtype == PRM_BF16 ? 2 : 4;
-  (void)wb;
   for (int i = 0; i < n_mats; ++i) {
     const int64_t m = rows[i], n = cols[i];
     if (m < 1 || n < 1 || m > kMaxDim || n > kMaxDim)

@@ -100,6 +100,7 @@ def test_workspace_fits_dit_configs():
     ("K", 0, prm.PRM_EINVAL), ("beta", 1.0, prm.PRM_EINVAL), ("beta", -0.1, prm.PRM_EINVAL),
     ("gamma", 0.0, prm.PRM_EINVAL), ("eps_rownorm", 0.0, prm.PRM_EINVAL),
     ("lr", -1.0, prm.PRM_EINVAL), ("wd", -0.5, prm.PRM_EINVAL), ("scale_mode", 7, prm.PRM_EINVAL),
+    ("eps_rownorm", float("inf"), prm.PRM_EINVAL), ("eps_ns", float("nan"), prm.PRM_EINVAL),
     ("param_dtype", 5, prm.PRM_EDTYPE), ("grad_dtype", -1, prm.PRM_EDTYPE),
     ("nesterov", 2, prm.PRM_EINVAL),
 ])
