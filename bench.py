@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--config", type=int, default=2,
                     help="workload index: 0 tiny, 1 DiT-1.3B, 2 DiT-4B (default), 3 DiT-9B, 4 DiT-15B")
     ap.add_argument("--K", type=int, default=None, help="refresh period (default: the workload's)")
+    ap.add_argument("--variant", action="append", default=[],
+                    choices=["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh"],
+                    help="ablation flags of the configuration (repeatable); the default is the paper's method")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel attribution period")
     ap.add_argument("--no-aux", action="store_true", help="skip timing the aux-group AdamW step")
@@ -264,7 +267,8 @@ def main():
     shapes = list(wl.shapes)
     dt = {"f32": prm.F32, "bf16": prm.BF16}
     cfg = prm.config_default(K=K, lr=wl.lr, wd=wl.wd, gamma=wl.gamma, beta=wl.beta,
-                             param_dtype=dt[wl.param_dtype], grad_dtype=dt[wl.grad_dtype])
+                             param_dtype=dt[wl.param_dtype], grad_dtype=dt[wl.grad_dtype],
+                             **{v: 1 for v in args.variant})
     log(f"[bench] workload {wl.name}: {len(shapes)} matrices, "
         f"{sum(m * n for m, n in shapes) / 1e9:.3f} G elements, K={K}, steps={steps}, warmup={warmup}")
     W, M, G = make_inputs(args.config, wl, dev)
@@ -421,7 +425,7 @@ def main():
         "config": {"workload": wl.name, "matrices": len(shapes), "elements": elems, "K": K,
                    "lr": wl.lr, "wd": wl.wd, "gamma": wl.gamma, "beta": wl.beta,
                    "param_dtype": wl.param_dtype, "grad_dtype": wl.grad_dtype, "momentum_dtype": "f32",
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU", "variants": args.variant},
         "refresh_ms": T_ref,
         "rowwise_ms": T_rw,
         "refresh_mfma_frac": refresh_mfma_frac,
