@@ -327,6 +327,24 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y, x, c, 0, 0, 0);
   };
 
+  // Fragments live across stages: the last NDEF row blocks of a stage's last
+  // k-step run after the stage barrier, from set 1, while the next stage's
+  // first fragments (set 0) load from LDS (measured 0.3% on the refresh step;
+  // deferring two row blocks is equal).  Set 1 starts at zero, so the first
+  // stage's deferred products add nothing.
+  constexpr int NDEF = 1;
+  bf16x8 fa[2][MI], fb[2][NI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i) fa[1][i] = bf16x8{};
+#pragma unroll
+  for (int j = 0; j < NI; ++j) fb[1][j] = bf16x8{};
+  auto deferred = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = MI - NDEF; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j) mfma(fa[1][i], fb[1][j], acc[i][j]);
+  };
+
   // Compute one stage from `cur` while streaming stage `knext` (if >= 0) into
   // `nxt`.  The vector-memory path accepts about one 1 KB wave load per 16
   // cycles, so the wave's loads are spread between MFMA sub-groups (a quarter
@@ -342,7 +360,6 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     const char* b = cur + A_BYTES;
     const int64_t kn = (int64_t)knext * BK;
     const bool more = knext >= 0;
-    bf16x8 fa[2][MI], fb[2][NI];
     // two transposing reads give lane L the column (L % 32) of the block at 8
     // consecutive k: k-rows 16 ks + 8 (L / 32) + 4 kk + s, s = 0..3
     auto rd_tn = [&](const char* base, const int (&off)[2], int ks) __attribute__((always_inline)) {
@@ -374,12 +391,13 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     for (int i = 0; i < MI; ++i) rda(0, i, 0);
 #pragma unroll
     for (int j = 0; j < NI; ++j) rdb(0, j, 0);
+    deferred();  // the previous stage's last row blocks (zeros before the first stage)
     __builtin_amdgcn_sched_barrier(0);
     auto kstep = [&](auto ksc) __attribute__((always_inline)) {
       constexpr int ks = decltype(ksc)::value;
       constexpr int cs = ks & 1;
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {          // sub-group: row block i, NI MFMAs
+      for (int i = 0; i < (ks == 3 ? MI - NDEF : MI); ++i) {  // sub-group: row block i, NI MFMAs
         if (ks < 3) {
           if (ks < PRM_DMA_KSTEPS && more) {
             const int slot = ks * MI + i;
@@ -444,6 +462,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     }
   }
 
+  deferred();
   // ---- epilogue ----
   // Final values are formed in registers, converted to bf16 and the whole
   // 256 x 256 tile is staged once in LDS (rows 0..127 in s0, 128..255 in s1;
