@@ -477,6 +477,20 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // Lane L holds output row 32 i + L % 32 of its wave block and, for block
   // column j and q = 0..3, the 4 columns 32 j + 8 q + 4 (L / 32) + 0..3.
   const bool diag = (KIND != GEMM_APPLY) && it.tm == it.tn;  // Gram / square tile on the diagonal
+  if constexpr (KIND == GEMM_POLY) {
+    // the square needs the Ao tile of its own output position: it enters the
+    // staging area (layout below) by 1 KB DMA wave loads, 2 tile rows each,
+    // and every lane later reads and overwrites its own 8 bytes in place
+#pragma unroll 4
+    for (int q = 0; q < BM / 2 / NWAVES; ++q) {
+      const int r2 = 2 * ((BM / 2 / NWAVES) * wave + q);  // first row of the pair (even)
+      const int R = r2 + (lane >> 5);
+      const int c = (lane & 31) ^ (R & 31);
+      __builtin_amdgcn_global_load_lds((const void*)(d.Ao + (row0 + R) * rp + col0 + 8 * c),
+                                       (lds_ptr)((r2 < 128 ? s0 : s1) + (r2 & 127) * 512), 16, 0, 0);
+    }
+    __syncthreads();
+  }
   const float alpha = (p.iter == 0) ? *d.alpha : 1.0f;
   const bool last = (KIND == GEMM_APPLY) && p.last;
   {
@@ -498,20 +512,11 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     }
 #pragma unroll
     for (int ih = 0; ih < MI; ih += 2) {
-      // square: Ao and dA of rows 32 i + L % 32 for two row blocks
-      uint2 ao[2][NI][4];
+      // square: dA of rows 32 i + L % 32 for two row blocks
       float drow[2];
       if constexpr (KIND == GEMM_POLY) {
 #pragma unroll
-        for (int ii = 0; ii < 2; ++ii) {
-          const int64_t gr = grow + 32 * (ih + ii);
-          drow[ii] = d.dA[gr];
-#pragma unroll
-          for (int j = 0; j < NI; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              ao[ii][j][q] = *reinterpret_cast<const uint2*>(d.Ao + gr * rp + gcol + 32 * j + 8 * q);
-        }
+        for (int ii = 0; ii < 2; ++ii) drow[ii] = d.dA[grow + 32 * (ih + ii)];
       }
 #pragma unroll
       for (int ii = 0; ii < 2; ++ii) {
@@ -529,7 +534,8 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
               for (int e = 0; e < 4; ++e) v[e] = s2 * acc[i][j][4 * q + e];
             } else if constexpr (KIND == GEMM_POLY) {
               // A^2 = dA^2 + dA Ao + Ao dA + Ao Ao;  B = b A + c A^2
-              const uint2 w2 = ao[ii][j][q];
+              const int ch0 = (wn * WN + 32 * j + 8 * q) >> 3;
+              const uint2 w2 = *reinterpret_cast<const uint2*>(trow + ((ch0 ^ (r & 31)) << 4));
               const float a4[4] = {bf2f(w2.x & 0xffffu), bf2f(w2.x >> 16), bf2f(w2.y & 0xffffu), bf2f(w2.y >> 16)};
 #pragma unroll
               for (int e = 0; e < 4; ++e)
