@@ -22,6 +22,7 @@ Only rank 0 at N = 1 runs; there is no multi-GPU path.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -52,6 +53,8 @@ def parse():
     ap.add_argument("--variant", action="append", default=[],
                     choices=["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh"],
                     help="ablation flags of the configuration (repeatable); the default is the paper's method")
+    ap.add_argument("--grad-dtype", choices=["bf16", "f32"], default=None,
+                    help="gradient storage dtype (default: the workload's, bf16 for the DiT-shaped sets)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel attribution period")
     ap.add_argument("--no-aux", action="store_true", help="skip timing the aux-group AdamW step")
@@ -259,6 +262,11 @@ def main():
     from oracle import prm_oracle as po
 
     wl = synth.WORKLOADS[args.config]
+    if args.grad_dtype and args.grad_dtype != wl.grad_dtype:
+        wl = dataclasses.replace(wl, grad_dtype=args.grad_dtype)
+    # the committed counter passes were taken on the workload's own
+    # configuration; a variant moves other bytes, so they are not attached
+    default_cfg = not args.variant and wl.grad_dtype == synth.WORKLOADS[args.config].grad_dtype
     K = args.K or wl.K
     steps = args.steps if args.steps is not None else 2 * K
     warmup = args.warmup if args.warmup is not None else K
@@ -350,11 +358,11 @@ def main():
         if rw_names:
             dom_rw = max(rw_names, key=lambda k: kernels[k]["total_ms"])
             roofline_rw = roof(dom_rw, kernels[dom_rw])
-        mf = counter_mfma(wl.name)
+        mf = counter_mfma(wl.name) if default_cfg else None
         if roofline is not None and mf and roofline["kernel"] in mf:
             roofline["mfma_busy_counters"] = mf[roofline["kernel"]]["mfma_busy"]
             roofline["shader_clock_ghz_counters"] = mf[roofline["kernel"]]["clock_ghz"]
-        traffic = counter_traffic(wl.name)
+        traffic = counter_traffic(wl.name) if default_cfg else None
         for rf in (roofline, roofline_rw):
             if rf is not None and traffic and rf["kernel"] in traffic:
                 tc = traffic[rf["kernel"]]
@@ -366,7 +374,7 @@ def main():
     aux = None
     if not args.no_aux and wl.name in synth.MUON_ROUTED:
         aux = aux_adamw(args.config, wl, dev, stream)
-        tr = counter_traffic(wl.name)
+        tr = counter_traffic(wl.name) if default_cfg else None
         if tr and "adamw" in tr:
             aux["roofline"]["traffic"] = tr["adamw"]["fetch_bytes_per_launch"] + tr["adamw"]["write_bytes_per_launch"]
             aux["roofline"]["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
@@ -381,16 +389,16 @@ def main():
         mf = prm.peak_mfma(50000)
         hb = prm.peak_hbm(4 << 30)
         rb, wrb = gb + 4 + wb, 4 + wb
-        if (gb, wb) == (2, 2):
-            mix = hb["rowwise_gbs"]
-        else:
-            # other dtypes: R read and Wr written bytes per element move at
-            # best at (R + Wr) / (R / read_rate + Wr / write_rate)
-            mix = (rb + wrb) / (rb / hb["read_gbs"] + wrb / hb["write_gbs"])
+        # the probe moves the bf16 mix (three read streams, two write
+        # streams); other dtypes have the same streams with wider elements and
+        # the step runs at the same byte rate with them (5.3 TB/s with fp32 G
+        # and with bf16 G at DiT-4B), so the probe is their ceiling too
+        mix = hb["rowwise_gbs"]
         peaks = {"mfma_bf16_tflops": mf["tflops"], "mfma_clock_ghz": mf["clock_ghz"],
                  "hbm_read_gbs": hb["read_gbs"], "hbm_write_gbs": hb["write_gbs"], "hbm_copy_gbs": hb["copy_gbs"],
                  "hbm_rowwise_probe_gbs": hb["rowwise_gbs"],
-                 "hbm_rowwise_mix_gbs": mix, "rowwise_mix": f"{rb} B read + {wrb} B written per element"}
+                 "hbm_rowwise_mix_gbs": mix,
+                 "rowwise_mix": f"step: {rb} B read + {wrb} B written per element; probe: 8 + 6"}
         log(f"[bench] measured ceilings: MFMA {mf['tflops']:.0f} TFLOP/s at {mf['clock_ghz']:.2f} GHz, "
             f"HBM read {hb['read_gbs']:.0f} / write {hb['write_gbs']:.0f} / copy {hb['copy_gbs']:.0f} / "
             f"row-wise traffic {hb['rowwise_gbs']:.0f} GB/s")

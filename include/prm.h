@@ -105,7 +105,9 @@ int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* 
 /* One optimizer step t (0-based, >= 0) over every matrix, enqueued on the
  * context's stream.  params[i]: W (param_dtype), grads[i]: G (grad_dtype),
  * momentum[i]: M (fp32); all device pointers, 16-byte aligned.  lr < 0 uses
- * cfg->lr.  *did_refresh (nullable) receives rho_t, computed on the host. */
+ * cfg->lr.  *did_refresh (nullable) receives rho_t, computed on the host.
+ * Runs on the device the context was created on; the caller's current device
+ * is restored before returning. */
 int prm_step(prm_ctx* ctx, void* const* params, const void* const* grads,
              float* const* momentum, int64_t step, float lr, int32_t* did_refresh);
 
@@ -165,7 +167,7 @@ int prm_destroy(prm_ctx* ctx);
  * and p is rounded to its storage type (RNE).  Tensors are DEVICE pointers to
  * contiguous arrays of numel[i] elements owned by the caller: p (param_dtype)
  * and the moments m, v (fp32) are updated in place, g (grad_dtype) is only
- * read; they must be 16-byte aligned and must not overlap.  Same stream and
+ * read; they must be 16-byte aligned and must not overlap.  Same stream, device and
  * error rules as prm_step (validation before anything is enqueued; the call
  * only enqueues, except that new pointer arrays wait for the previous call's
  * small pointer-table upload). */

@@ -46,6 +46,23 @@ int fail(int code, const char* fmt, ...) {
 constexpr uint64_t kAutoBudget = 32ull << 30;  // NS5 chunk workspace cap when unset
 constexpr int64_t kMaxDim = 1ll << 24;
 
+// Makes the context's device current for one entry point and restores the
+// caller's device when the call returns.
+struct DeviceScope {
+  int prev = -1;
+  hipError_t enter(int dev) {
+    hipError_t e = hipGetDevice(&prev);
+    if (e != hipSuccess) {
+      prev = -1;
+      return e;
+    }
+    return prev == dev ? hipSuccess : hipSetDevice(dev);
+  }
+  ~DeviceScope() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
 
@@ -572,7 +589,8 @@ int do_step(prm_ctx* c, void* const* params, const void* const* grads, float* co
   const int rho = c->cfg.never_refresh ? 0 : (t % c->cfg.K == 0 ? 1 : 0);
   if (did_refresh) *did_refresh = rho;
   if (n == 0) return PRM_OK;
-  HIP_TRY(hipSetDevice(c->device));
+  DeviceScope dev;
+  HIP_TRY(dev.enter(c->device));
   int rc = upload_desc(c, params, grads, momentum, debug ? dirs : nullptr);
   if (rc) return rc;
   return rho ? refresh_step(c, eta, debug) : rowwise_step(c, eta, debug);
@@ -858,7 +876,8 @@ int prm_adamw_step(prm_adamw_ctx* c, void* const* params, const void* const* gra
     same = same && d.P == params[i] && d.G == grads[i] && d.M == exp_avg[i] && d.V == exp_avg_sq[i];
   }
   if (c->nchunks == 0) return PRM_OK;
-  HIP_TRY(hipSetDevice(c->device));
+  DeviceScope dev;
+  HIP_TRY(dev.enter(c->device));
   if (!same) {
     if (c->uploaded) HIP_TRY(hipEventSynchronize(c->upload_done));
     for (int i = 0; i < n; ++i) {
