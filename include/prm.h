@@ -19,8 +19,9 @@
  *   W <- (1 - eta*lambda)*W - eta*D     (eq. periodic-direction; Alg. 1)
  *
  * Numerics: momentum, RowNorm and the parameter write are fp32; NS5 runs as
- * bf16-input / fp32-accumulate matrix products (MFMA) with the Gram matrix
- * carried as a bf16 hi + lo pair; W is rounded to its storage type (RNE).
+ * bf16-input / fp32-accumulate matrix products (MFMA), with the diagonals of
+ * G and B carried in fp32 and only their off-diagonal parts rounded to bf16
+ * for the next product; W is rounded to its storage type (RNE).
  *
  * Memory: every matrix buffer is a DEVICE pointer to a contiguous row-major
  * m x n array owned by the caller.  W and M are updated in place, G is only

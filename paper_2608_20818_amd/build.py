@@ -68,5 +68,29 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+C_CALLER_SRC = os.path.join(ROOT, "tests", "c_caller.c")
+C_CALLER_LIB = os.path.join(ROOT, "tests", "libc_caller.so")
+
+
+def build_c_caller() -> str:
+    """The plain-C caller of the C ABI used by the GPU tests (gcc, no device
+    code): tests/c_caller.c -> tests/libc_caller.so, linked to libprm.so and the
+    HIP runtime."""
+    cc = shutil.which("gcc") or "gcc"
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    tmp = C_CALLER_LIB + ".tmp"
+    cmd = [cc, "-std=c11", "-O2", "-Wall", "-Wextra", "-shared", "-fPIC", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(ROOT, "include"), "-I", os.path.join(rocm, "include"),
+           C_CALLER_SRC, "-o", tmp, "-L", HERE, "-lprm", "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+           f"-Wl,-rpath,$ORIGIN/../{os.path.basename(HERE)}", f"-Wl,-rpath,{os.path.join(rocm, 'lib')}"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        print(r.stdout, r.stderr, file=sys.stderr)
+        raise RuntimeError("gcc failed for tests/c_caller.c")
+    os.replace(tmp, C_CALLER_LIB)
+    return C_CALLER_LIB
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
+    print(build_c_caller())

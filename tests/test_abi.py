@@ -195,3 +195,23 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_c_caller_reports_bad_cases_before_touching_the_device(tmp_path):
+    # the plain-C caller the GPU tests use: it builds, binds to libprm and
+    # rejects unreadable or malformed cases before any HIP call
+    lib = os.path.join(ROOT, "tests", "libc_caller.so")
+    assert os.path.exists(lib), "run __graft_entry__.build()"
+    prm.load()
+    L = ctypes.CDLL(lib)
+    L.prm_c_run_case.argtypes = [ctypes.c_char_p, ctypes.c_char_p, ctypes.c_int]
+    L.prm_c_run_case.restype = ctypes.c_int
+    msg = ctypes.create_string_buffer(256)
+    assert L.prm_c_run_case(str(tmp_path / "absent").encode(), msg, len(msg)) == -1
+    assert "cannot open" in msg.value.decode()
+    (tmp_path / "case.txt").write_text("2 5 1\n")
+    assert L.prm_c_run_case(str(tmp_path).encode(), msg, len(msg)) == -1
+    assert "malformed" in msg.value.decode()
+    needed = subprocess.run(["readelf", "-d", lib], capture_output=True, text=True, check=True).stdout
+    assert "libprm.so" in needed and "libamdhip64" in needed
+    assert "libtorch" not in needed and "python" not in needed
