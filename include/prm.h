@@ -210,7 +210,8 @@ int prm_adamw_destroy(prm_adamw_ctx* ctx);
  *
  * prm_peak_mfma: sustained bf16 MFMA rate.  Every wave runs 8 independent
  * 32x32x16 accumulator chains for `iters` iterations (1 <= iters <= 2^24; 16
- * waves per compute unit, no memory traffic).  *tflops = executed FLOPs over
+ * waves per compute unit, no memory traffic) on pseudo-random operands that
+ * change from one MFMA to the next, as a GEMM's do.  *tflops = executed FLOPs over
  * the HIP-event time; *clock_ghz = the shader clock during the loop (shader
  * cycles over 100 MHz reference ticks), which drops below the nominal
  * 2.4 GHz when the power limit is reached.

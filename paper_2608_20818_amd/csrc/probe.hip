@@ -11,15 +11,24 @@ typedef __bf16 pbf16x8 __attribute__((ext_vector_type(8)));
 typedef float pfloatx16 __attribute__((ext_vector_type(16)));
 
 // Every wave runs 8 independent accumulator chains, so the MFMA pipe never
-// waits on a result; operands stay in registers (no memory traffic).
+// waits on a result; operands stay in registers (no memory traffic).  The
+// operands are 4 sets of pseudo-random values in [-1, 1) and consecutive MFMAs
+// take different ones, as in a GEMM: the power drawn, and with it the clock
+// the power limit allows, depends on how much the operand bits toggle (fixed
+// operands run about 10% faster, an optimistic ceiling).
 __global__ __launch_bounds__(256) void probe_mfma_kernel(float* sink, unsigned long long* clk, int iters) {
   const int lane = threadIdx.x & 63;
-  pbf16x8 a, b;
+  pbf16x8 a[4], b[4];
+  unsigned h = 2654435761u * (unsigned)(lane + 1) + 97u * blockIdx.x;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    a[e] = (__bf16)(0.001f * (float)(lane + e));
-    b[e] = (__bf16)(0.002f * (float)(lane - e));
-  }
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      h = h * 1664525u + 1013904223u;
+      a[s][e] = (__bf16)((float)((int)(h >> 8) - (1 << 23)) * (1.0f / (1 << 23)));
+      h = h * 1664525u + 1013904223u;
+      b[s][e] = (__bf16)((float)((int)(h >> 8) - (1 << 23)) * (1.0f / (1 << 23)));
+    }
   pfloatx16 c[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j)
@@ -28,7 +37,8 @@ __global__ __launch_bounds__(256) void probe_mfma_kernel(float* sink, unsigned l
   const unsigned long long t0 = __builtin_amdgcn_s_memtime(), r0 = __builtin_amdgcn_s_memrealtime();
   for (int i = 0; i < iters; ++i) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c[j], 0, 0, 0);
+    for (int j = 0; j < 8; ++j)
+      c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(j >> 1) & 3], b[j & 3], c[j], 0, 0, 0);
   }
   const unsigned long long t1 = __builtin_amdgcn_s_memtime(), r1 = __builtin_amdgcn_s_memrealtime();
   float s = 0.f;
