@@ -237,35 +237,48 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // KR wave + 2 q + lane / 32 (KR = KROWS_PER_WAVE, a multiple of 4) and lane
   // fills physical chunk lane % 32, i.e. logical chunk (lane % 32) ^ swz_tn_f(k-row).
   static_assert(ROWS_PER_WAVE % 16 == 0 && KROWS_PER_WAVE % 4 == 0, "swizzle phase per wave");
-  const uint16_t *srcA, *srcB;
+  // Each wave load is addressed as a wave-uniform base (scalar registers: the
+  // operand, the tile, the wave and the k offset) plus a 32-bit per-lane byte
+  // offset fixed for the whole tile (the row or k-row, and the swizzled chunk),
+  // so issuing a load takes no 64-bit vector address arithmetic.  The offsets
+  // stay below 2^31 (at most 64 rows of 2^24 bf16).
+  const char *baseA, *baseB;
+  uint32_t voff[DMA_PER_WAVE];
   if constexpr (TN) {
-    srcA = P + (int64_t)(KROWS_PER_WAVE * wave + (lane >> 5)) * ld + row0;
-    srcB = Q + (int64_t)(KROWS_PER_WAVE * wave + (lane >> 5)) * ld + col0;
+    baseA = reinterpret_cast<const char*>(P + (int64_t)(KROWS_PER_WAVE * wave) * ld + row0);
+    baseB = reinterpret_cast<const char*>(Q + (int64_t)(KROWS_PER_WAVE * wave) * ld + col0);
+#pragma unroll
+    for (int qq = 0; qq < DMA_PER_WAVE; ++qq) {
+      const int krow = 2 * qq + (lane >> 5);  // + KR wave, which is 0 mod 4
+      voff[qq] = (uint32_t)((krow * ld + (((lane & 31) ^ swz_tn_f(krow)) << 3)) * 2);
+    }
   } else {
+    baseA = reinterpret_cast<const char*>(P + (row0 + ROWS_PER_WAVE * wave) * ld);
+    baseB = reinterpret_cast<const char*>(Q + (col0 + ROWS_PER_WAVE * wave) * ld);
     // swz_f(row) = 4 (q % 2) + lane / 16, so the lane's source chunk only
-    // depends on the parity of q
+    // depends on the parity of q: chunk bit 2 flips for odd q, i.e.
+    // (c ^ 4) * 8 elements = c * 8 +- 32
     const int64_t lane_off = (int64_t)(lane >> 3) * ld + (((lane & 7) ^ (lane >> 4)) << 3);
-    srcA = P + (row0 + ROWS_PER_WAVE * wave) * ld + lane_off;
-    srcB = Q + (col0 + ROWS_PER_WAVE * wave) * ld + lane_off;
+#pragma unroll
+    for (int qq = 0; qq < DMA_PER_WAVE; ++qq) {
+      const int flip = (qq & 1) ? ((lane & 4) ? -32 : 32) : 0;
+      voff[qq] = (uint32_t)((lane_off + (int64_t)(8 * qq) * ld + flip) * 2);
+    }
   }
   // One 1 KB wave load of the stage at k offset `k`: block q < DMA_PER_WAVE of
-  // operand A, the others of operand B.
+  // operand A, the others of operand B.  Written as assembly because the
+  // compiler folds the lane offset into a 64-bit vector address before adding
+  // k (two 64-bit vector adds per load in the main loop, measured 3% of the
+  // refresh step).  The compiler then does not see these LDS writes: every
+  // stage wait below is an explicit vmcnt(0) before the barrier.
   auto dma1 = [&](char* stage, int64_t k, int q) __attribute__((always_inline)) {
     const bool isb = q >= DMA_PER_WAVE;
     const int qq = isb ? q - DMA_PER_WAVE : q;
-    const uint16_t* src;
-    if constexpr (TN) {
-      const int krow = 2 * qq + (lane >> 5);  // + KR wave, which is 0 mod 4
-      src = (isb ? srcB : srcA) + (k + 2 * qq) * ld + (((lane & 31) ^ swz_tn_f(krow)) << 3);
-    } else {
-      // chunk bit 2 flips for odd q: (c ^ 4) * 8 elements = c * 8 +- 32
-      const int flip = (qq & 1) ? ((lane & 4) ? -32 : 32) : 0;
-      src = (isb ? srcB : srcA) + (int64_t)(8 * qq) * ld + k + flip;
-    }
-    __builtin_amdgcn_global_load_lds((const void*)src,
-                                     (lds_ptr)(stage + (isb ? A_BYTES : 0) + (DMA_PER_WAVE * wave + qq) * 1024),
-                                     16, 0, 0);
+    const char* base = (isb ? baseB : baseA) + (TN ? k * ld : k) * 2;
+    const uint32_t lds = (uint32_t)(uintptr_t)(lds_ptr)(stage + (isb ? A_BYTES : 0) + (DMA_PER_WAVE * wave + qq) * 1024);
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff[qq]), "s"(base), "s"(lds) : "m0");
   };
+  auto stage_landed = [&]() __attribute__((always_inline)) { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
 
   floatx16 acc[MI][NI];
 #pragma unroll
@@ -435,11 +448,14 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // stage 0 up front, then ping-pong: s0 holds even stages, s1 odd ones
 #pragma unroll
   for (int q = 0; q < NDMA; ++q) dma1(s0, 0, q);
+  stage_landed();
   __syncthreads();
   auto stage_pair = [&](int kt, auto f0, auto f1, bool fold0, bool fold1) __attribute__((always_inline)) {
     stage_compute(s0, s1, kt + 1, f0, fold0);
+    stage_landed();
     __syncthreads();  // stage kt+1 has landed; every wave is done with s0
     stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1, f1, fold1);
+    stage_landed();
     __syncthreads();
   };
   constexpr std::integral_constant<int, 0> nofold{};
