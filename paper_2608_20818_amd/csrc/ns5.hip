@@ -367,12 +367,15 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // FOLD (apply): 0 none; f >= 1: the stage holds this wave's output block
   // columns 2 (f - 1) and 2 (f - 1) + 1 as k
   // (one stage per wave, WN == BK): `fold` selects it at run time instead
-  auto stage_compute = [&](const char* cur, char* nxt, int knext, auto foldc, bool fold) __attribute__((always_inline)) {
+  // MORE: 1 a next stage exists, 0 none (the tile's last stage), -1 decided at
+  // run time from knext; static where possible, so the main loop has no branch
+  auto stage_compute = [&](const char* cur, char* nxt, int knext, auto foldc, bool fold, auto morec) __attribute__((always_inline)) {
     constexpr int FOLD = decltype(foldc)::value;
+    constexpr int MORE = decltype(morec)::value;
     const char* a = cur;
     const char* b = cur + A_BYTES;
     const int64_t kn = (int64_t)knext * BK;
-    const bool more = knext >= 0;
+    const bool more = MORE == 1 || (MORE == -1 && knext >= 0);
     // two transposing reads give lane L the column (L % 32) of the block at 8
     // consecutive k: k-rows 16 ks + 8 (L / 32) + 4 kk + s, s = 0..3
     auto rd_tn = [&](const char* base, const int (&off)[2], int ks) __attribute__((always_inline)) {
@@ -450,11 +453,16 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   for (int q = 0; q < NDMA; ++q) dma1(s0, 0, q);
   stage_landed();
   __syncthreads();
-  auto stage_pair = [&](int kt, auto f0, auto f1, bool fold0, bool fold1) __attribute__((always_inline)) {
-    stage_compute(s0, s1, kt + 1, f0, fold0);
+  constexpr std::integral_constant<int, 1> more_yes{};
+  constexpr std::integral_constant<int, 0> more_no{};
+  constexpr std::integral_constant<int, -1> more_rt{};
+  // stages kt (in s0) and kt + 1 (in s1); nk is even, so stage kt + 1 exists,
+  // and m1 says whether stage kt + 2 does
+  auto stage_pair = [&](int kt, auto f0, auto f1, bool fold0, bool fold1, auto m1) __attribute__((always_inline)) {
+    stage_compute(s0, s1, kt + 1, f0, fold0, more_yes);
     stage_landed();
     __syncthreads();  // stage kt+1 has landed; every wave is done with s0
-    stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1, f1, fold1);
+    stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1, f1, fold1, m1);
     stage_landed();
     __syncthreads();
   };
@@ -465,17 +473,20 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   if constexpr (KIND == GEMM_APPLY && WN == BK) {
     // one stage: a run-time flag in a single loop (J is static either way)
     constexpr std::integral_constant<int, -1> fold_rt{};
-    for (; kt < nk; kt += 2) stage_pair(kt, fold_rt, fold_rt, kt == kfold, kt + 1 == kfold);
+    for (; kt < nk; kt += 2) stage_pair(kt, fold_rt, fold_rt, kt == kfold, kt + 1 == kfold, more_rt);
   } else {
     // two stages (a stage pair): it runs between two plain loops, since one
-    // loop body holding both variants spills
-    for (; kt < (kfold & ~1); kt += 2) stage_pair(kt, nofold, nofold, false, false);
+    // loop body holding both variants spills.  The pairs before the last one
+    // always stream a next stage; the last pair (kt = nk - 2) runs on its own.
+    const int kfirst = (KIND == GEMM_APPLY) ? (kfold & ~1) : nk - 2;  // kfold < nk
+    for (; kt < kfirst; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
     if constexpr (KIND == GEMM_APPLY) {
       static_assert(WN == 2 * BK, "a wave's output columns span one or two stages");
-      stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, true, true);
+      stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, true, true, more_rt);
       kt += 2;
-      for (; kt < nk; kt += 2) stage_pair(kt, nofold, nofold, false, false);
+      for (; kt < nk - 2; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
     }
+    if (kt < nk) stage_pair(kt, nofold, nofold, false, false, more_no);
   }
 
   deferred();
