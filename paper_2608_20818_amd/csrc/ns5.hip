@@ -270,13 +270,20 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // compiler folds the lane offset into a 64-bit vector address before adding
   // k (two 64-bit vector adds per load in the main loop, measured 3% of the
   // refresh step).  The compiler then does not see these LDS writes: every
-  // stage wait below is an explicit vmcnt(0) before the barrier.
+  // stage wait below is an explicit vmcnt(0) before the barrier.  M0 (the LDS
+  // destination of the DMA) is a register the compiler reserves and does not
+  // save around the asm; in these kernels its own code reads M0 only for the
+  // square epilogue's LDS DMA and writes it right before each such read (the
+  // compiled assembly is checked for this by tests/test_abi.py).
   auto dma1 = [&](char* stage, int64_t k, int q) __attribute__((always_inline)) {
     const bool isb = q >= DMA_PER_WAVE;
     const int qq = isb ? q - DMA_PER_WAVE : q;
     const char* base = (isb ? baseB : baseA) + (TN ? k * ld : k) * 2;
     const uint32_t lds = (uint32_t)(uintptr_t)(lds_ptr)(stage + (isb ? A_BYTES : 0) + (DMA_PER_WAVE * wave + qq) * 1024);
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"  // the M0 clobber, see above
     asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff[qq]), "s"(base), "s"(lds) : "m0");
+#pragma clang diagnostic pop
   };
   auto stage_landed = [&]() __attribute__((always_inline)) { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
 

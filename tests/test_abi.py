@@ -215,3 +215,69 @@ def test_c_caller_reports_bad_cases_before_touching_the_device(tmp_path):
     needed = subprocess.run(["readelf", "-d", lib], capture_output=True, text=True, check=True).stdout
     assert "libprm.so" in needed and "libamdhip64" in needed
     assert "libtorch" not in needed and "python" not in needed
+
+
+def _m0_check(asm_text):
+    """(compiler LDS DMAs, inline-asm LDS DMAs, violations): a violation is an
+    M0 read the compiler emitted without its own M0 write before it in the
+    same basic block with no inline asm in between, or any other M0 reader."""
+    other_m0_readers = re.compile(r"^(s_movrel|v_movrel|s_sendmsg|ds_gws|v_interp|s_set_gpr_idx)")
+    compiler_m0 = False  # M0 holds a value the compiler wrote, with no asm since
+    in_asm = False
+    readers = asm_dma = 0
+    bad = []
+    for line in asm_text.splitlines():
+        s = line.strip()
+        if s.startswith(";;#ASMSTART"):
+            in_asm = True
+            continue
+        if s.startswith(";;#ASMEND"):
+            in_asm = False
+            continue
+        if re.match(r"^(\.LBB\w*|_Z\w+):", s):
+            compiler_m0 = False  # a new basic block or function: nothing is known
+            continue
+        if not s or s.startswith(";") or s.startswith("."):
+            continue
+        writes_m0 = re.match(r"^s_\w+\s+m0,", s) is not None
+        if in_asm:
+            asm_dma += "global_load_lds" in s
+            if writes_m0:
+                compiler_m0 = False
+            continue
+        if other_m0_readers.match(s):
+            bad.append(s)
+        if "global_load_lds" in s or re.search(r"buffer_load\w*.*\blds\b", s):
+            readers += 1
+            if not compiler_m0:
+                bad.append(s)
+        if writes_m0:
+            compiler_m0 = True
+    return readers, asm_dma, bad
+
+
+def test_m0_check_flags_a_planted_violation():
+    ok = "_Zk:\n s_mov_b32 m0, s1\n global_load_lds_dwordx4 v[0:1], off\n"
+    assert _m0_check(ok) == (1, 0, [])
+    planted = ("_Zk:\n s_mov_b32 m0, s1\n ;;#ASMSTART\n s_mov_b32 m0, s2\n global_load_lds_dwordx4 v1, s[2:3]\n"
+               " ;;#ASMEND\n global_load_lds_dwordx4 v[0:1], off\n")
+    assert len(_m0_check(planted)[2]) == 1
+    assert len(_m0_check("_Zk:\n s_mov_b32 m0, s1\n.LBB0_1:\n global_load_lds_dwordx4 v[0:1], off\n")[2]) == 1
+    assert len(_m0_check("_Zk:\n s_sendmsg sendmsg(MSG_DEALLOC_VGPRS)\n")[2]) == 1
+
+
+def test_gemm_inline_dma_leaves_m0_to_the_compiler(tmp_path):
+    # The NS5 GEMM issues its stage loads through inline assembly that writes
+    # M0, a register the compiler reserves and does not save around asm.  That
+    # is sound only while every M0 read the compiler emits itself follows its
+    # own M0 write in the same basic block with no asm in between.
+    from paper_2608_20818_amd import build as b
+    out = tmp_path / "ns5.s"
+    r = subprocess.run([b.hipcc(), f"--offload-arch={b.ARCH}", "-O3", "-std=c++17", "-Xclang", "-target-feature",
+                        "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"), "-I", b.CSRC,
+                        "--cuda-device-only", "-S", os.path.join(b.CSRC, "ns5.hip"), "-o", str(out)],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    readers, asm_dma, bad = _m0_check(out.read_text())
+    assert asm_dma > 0 and readers > 0
+    assert not bad, bad[:5]
