@@ -278,3 +278,18 @@ def test_long_rows_and_columns(t):
     rho, res = run_one_step(shapes, cfg, t, workload_id=98)
     assert rho == (1 if t == 0 else 0)
     check(res, rho, cfg, shapes, cfg.lr)
+
+
+@pytest.mark.parametrize("t", [0, 1])
+def test_largest_dimension(t):
+    # the largest dimension the ABI accepts (2^24) on both sides: a 1 x 2^24
+    # row (generic row-wise kernel; a Gram whose one tile streams 262144 K
+    # stages; 65536 apply tiles) and a 2^24 x 1 column (scalar tall path with
+    # 524288 row blocks of partial sums)
+    n = 1 << 24
+    shapes = [(1, n), (n, 1)]
+    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=prm.BF16, grad_dtype=prm.BF16)
+    rho, res = run_one_step(shapes, cfg, t, workload_id=99)
+    assert rho == (1 if t == 0 else 0)
+    check(res, rho, cfg, shapes, cfg.lr)
+    torch.cuda.empty_cache()
