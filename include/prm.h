@@ -38,7 +38,10 @@
  * Errors: every entry point returns PRM_OK (0) or a negative PRM_E* code and
  * stores a message readable with prm_last_error() (per thread).  Arguments are
  * validated before anything is enqueued, so a failed call has no effect on
- * the caller's buffers.  A context is not thread-safe; separate contexts are.
+ * the caller's buffers.  Buffer pointers that differ from the previous call's
+ * are checked with hipPointerGetAttributes: host memory, or memory of another
+ * device than the context's, is refused with PRM_EINVAL (a kernel reading it
+ * would fault).  A context is not thread-safe; separate contexts are.
  */
 #ifndef PRM_H
 #define PRM_H
@@ -51,7 +54,7 @@ extern "C" {
 #endif
 
 #define PRM_OK 0
-#define PRM_EINVAL (-1)  /* bad argument: K < 1, beta outside [0,1), shape < 1, NULL, t < 0, ... */
+#define PRM_EINVAL (-1)  /* bad argument: K < 1, beta outside [0,1), shape < 1, NULL, host pointer, t < 0, ... */
 #define PRM_EDTYPE (-2)  /* unsupported storage type */
 #define PRM_EALIGN (-3)  /* a device pointer is not 16-byte aligned */
 #define PRM_ENOMEM (-4)  /* workspace does not fit the budget or the device */

@@ -204,6 +204,8 @@ class Optimizer:
         for i, (x, s) in enumerate(zip(xs, self.shapes)):
             if x is None or isinstance(x, int):
                 continue
+            if not x.is_cuda:
+                raise ValueError(f"{what}[{i}]: need a device tensor, got one on {x.device}")
             if tuple(x.shape) != s or not x.is_contiguous() or str(x.dtype) != f"torch.{dtype_name}":
                 raise ValueError(f"{what}[{i}]: need contiguous {dtype_name} {s}, got "
                                  f"{x.dtype} {tuple(x.shape)} contiguous={x.is_contiguous()}")
@@ -289,6 +291,8 @@ class AuxAdamW:
         for i, (x, k) in enumerate(zip(xs, self.numels)):
             if x is None or isinstance(x, int):
                 continue
+            if not x.is_cuda:
+                raise ValueError(f"{what}[{i}]: need a device tensor, got one on {x.device}")
             if x.numel() != k or not x.is_contiguous() or str(x.dtype) != f"torch.{dtype_name}":
                 raise ValueError(f"{what}[{i}]: need contiguous {dtype_name} with {k} elements, got "
                                  f"{x.dtype} {x.numel()} contiguous={x.is_contiguous()}")

@@ -63,6 +63,24 @@ struct DeviceScope {
   }
 };
 
+// A caller buffer must be memory of the context's device (or managed
+// memory): a host pointer handed to a kernel faults the GPU, so it is refused
+// before anything is enqueued.  Checked when a pointer differs from the one
+// the previous call passed at the same position.
+int check_device_ptr(int dev, const void* p, const char* what, int i, int k) {
+  hipPointerAttribute_t a;
+  hipError_t e = hipPointerGetAttributes(&a, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(PRM_EINVAL, "%s %d: pointer %d is not device memory (%s)", what, i, k, hipGetErrorString(e));
+  }
+  if (a.type == hipMemoryTypeManaged || (a.type == hipMemoryTypeDevice && a.device == dev)) return PRM_OK;
+  if (a.type == hipMemoryTypeDevice)
+    return fail(PRM_EINVAL, "%s %d: pointer %d is memory of device %d, the context runs on device %d", what, i, k,
+                a.device, dev);
+  return fail(PRM_EINVAL, "%s %d: pointer %d is host memory; device memory is required", what, i, k);
+}
+
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
 
@@ -584,6 +602,10 @@ int do_step(prm_ctx* c, void* const* params, const void* const* grads, float* co
       if (!ps[k] && k == 3) continue;  // direction not wanted for this matrix
       if (!ps[k]) return fail(PRM_EINVAL, "matrix %d: NULL device pointer (argument %d)", i, k);
       if ((uintptr_t)ps[k] % 16) return fail(PRM_EALIGN, "matrix %d: pointer %d is not 16-byte aligned", i, k);
+      if (!c->uploaded || c->last_ptrs[4 * i + k] != ps[k]) {
+        const int rc = check_device_ptr(c->device, ps[k], "matrix", i, k);
+        if (rc) return rc;
+      }
     }
   }
   const int rho = c->cfg.never_refresh ? 0 : (t % c->cfg.K == 0 ? 1 : 0);
@@ -873,6 +895,13 @@ int prm_adamw_step(prm_adamw_ctx* c, void* const* params, const void* const* gra
       if ((uintptr_t)ps[k] % 16) return fail(PRM_EALIGN, "tensor %d: pointer %d is not 16-byte aligned", i, k);
     }
     const AuxDesc& d = c->desc[i];
+    const void* prev[4] = {d.P, d.G, d.M, d.V};
+    for (int k = 0; k < 4; ++k) {
+      if (!c->uploaded || prev[k] != ps[k]) {
+        const int rc = check_device_ptr(c->device, ps[k], "tensor", i, k);
+        if (rc) return rc;
+      }
+    }
     same = same && d.P == params[i] && d.G == grads[i] && d.M == exp_avg[i] && d.V == exp_avg_sq[i];
   }
   if (c->nchunks == 0) return PRM_OK;

@@ -241,6 +241,36 @@ def test_misaligned_pointer_rejected_without_side_effects():
     assert torch.equal(M, torch.ones_like(M))
 
 
+def test_host_pointers_rejected_before_any_launch():
+    # host memory (pageable or pinned) where device memory is required: the
+    # library refuses it before enqueuing anything (a kernel would fault)
+    import numpy as np
+    shapes = [(8, 16)]
+    cfg = prm.config_default(param_dtype=0, grad_dtype=0)
+    G = torch.ones(8, 16, device="cuda")
+    M = torch.ones(8, 16, device="cuda")
+    W = torch.zeros(8, 16, device="cuda")
+    pageable = np.zeros(8 * 16 + 16, dtype=np.float32)
+    addr = pageable.ctypes.data
+    addr += (-addr) % 16  # aligned, so only the memory kind is wrong
+    pinned = torch.zeros(8, 16, dtype=torch.float32).pin_memory()
+    with prm.Optimizer(shapes, cfg) as opt:
+        for bad in (addr, pinned.data_ptr()):
+            with pytest.raises(prm.PRMError) as e:
+                opt.step([W], [G], [bad], 0)
+            assert e.value.code == prm.PRM_EINVAL and "host memory" in str(e.value), str(e.value)
+        with pytest.raises(ValueError):
+            opt.step([W.cpu()], [G], [M], 0)  # the binding refuses a CPU tensor itself
+        opt.step([W], [G], [M], 1)  # valid pointers after the refusals
+    torch.cuda.synchronize()
+    assert torch.equal(G, torch.ones_like(G))
+    with prm.AuxAdamW([128], prm.adamw_config_default(param_dtype=0, grad_dtype=0)) as aux:
+        flat = [t.view(-1) for t in (W, G, M)]
+        with pytest.raises(prm.PRMError) as e:
+            aux.step([flat[0]], [flat[1]], [flat[2]], [pinned.data_ptr()], 1)
+        assert e.value.code == prm.PRM_EINVAL
+
+
 @pytest.mark.parametrize("t", [0, 1])
 def test_debug_step_with_some_directions_skipped(t):
     # NULL direction entries: those matrices' D is not written; W, M and the
