@@ -119,6 +119,27 @@ def counter_mfma(workload: str):
     return t["classes"]
 
 
+def executed_ns5_flops(shapes):
+    """FLOPs the NS5 GEMM kernels execute in one refresh step (MFMA work
+    actually issued), as opposed to the algorithmic 20 r^2 c + 10 r^3: every
+    matrix is padded to 256 x 256 tiles; the Gram and the square compute only
+    the tiles on and above the diagonal (T (T + 1) / 2 of T^2); the apply runs
+    every tile plus, per wave, 64 MFMAs for the diagonal term a X + dB X
+    against 64 nk regular ones (nk = rp / 64 stages of K)."""
+    tile = 256
+    total = {"ns_gram": 0.0, "ns_poly": 0.0, "ns_apply": 0.0}
+    for m, n in shapes:
+        r, c = min(m, n), max(m, n)
+        rp, cp = -(-r // tile) * tile, -(-c // tile) * tile
+        T = rp // tile
+        upper = T * (T + 1) // 2
+        nk = rp // 64
+        total["ns_gram"] += 5 * upper * 2.0 * tile * tile * cp
+        total["ns_poly"] += 5 * upper * 2.0 * tile * tile * rp
+        total["ns_apply"] += 5 * (cp // tile) * T * 2.0 * tile * tile * rp * (1 + 1 / nk)
+    return total
+
+
 def make_inputs(wl_idx, wl, device):
     import torch
     import synth
@@ -185,11 +206,14 @@ def aux_adamw(wl_idx, wl, dev, stream, steps: int = 50, warmup: int = 5):
 
 
 def cpu_baseline(wl_idx, wl, K, cfg_vals, budget_s: float = 12.0):
-    """Time the fp64 oracle on a bounded sample of the workload (about
-    `budget_s` of host work) and scale it to one optimizer step of the whole
-    weight set: refresh steps on whole matrices of the distinct shapes, cheapest
-    first, scaled by NS5 FLOPs; row-wise steps on 256 full oriented rows of every
-    distinct shape, scaled by elements."""
+    """Time the fp64 oracle on a bounded sample of the workload and scale it to
+    one optimizer step of the whole weight set: refresh steps on whole
+    matrices of the distinct shapes, cheapest first, until about `budget_s` of
+    host work, scaled by NS5 FLOPs; row-wise steps on 256 full oriented rows of
+    every distinct shape, scaled by elements.  The linear scaling is then
+    checked on the largest shape: one whole refresh step and one whole
+    row-wise step of it are timed too, and their times are reported against
+    what the sample's rates predict (and enter the sample)."""
     import synth
     from oracle import prm_oracle as po
     try:
@@ -202,6 +226,15 @@ def cpu_baseline(wl_idx, wl, K, cfg_vals, budget_s: float = 12.0):
     shapes = list(wl.shapes)
     distinct = sorted(set(shapes), key=lambda s: po.ns5_flops(*s))
     first = {s: shapes.index(s) for s in distinct}
+
+    def whole(m, n, t):
+        i = first[(m, n)]
+        w, mm, g = synth.host_matrix(wl_idx, i, m, n, synth.rank_of(wl, m, n), param_dtype=wl.param_dtype,
+                                     grad_dtype=wl.grad_dtype, beta=wl.beta, steps=(t,))
+        t0 = time.perf_counter()
+        po.step_matrix(w, mm, g[t], t, oc)
+        return time.perf_counter() - t0
+
     # row-wise: 256 oriented rows of each distinct shape
     t_rw, rw_elems, rw_desc = 0.0, 0, []
     for j, (m, n) in enumerate(distinct):
@@ -216,18 +249,27 @@ def cpu_baseline(wl_idx, wl, K, cfg_vals, budget_s: float = 12.0):
         rw_desc.append(f"{sm}x{sn}")
     # refresh: whole matrices, cheapest shapes first, until the budget is spent
     t_ns, ns_flops, ns_desc = 0.0, 0, []
-    for (m, n) in distinct:
-        i = first[(m, n)]
-        w, mm, g = synth.host_matrix(wl_idx, i, m, n, synth.rank_of(wl, m, n), param_dtype=wl.param_dtype,
-                                     grad_dtype=wl.grad_dtype, beta=wl.beta, steps=(0,))
-        t0 = time.perf_counter()
-        po.step_matrix(w, mm, g[0], 0, oc)
-        dt = time.perf_counter() - t0
+    largest = distinct[-1]
+    for (m, n) in distinct[:-1]:
+        dt = whole(m, n, 0)
         t_ns += dt
         ns_flops += po.ns5_flops(m, n)
         ns_desc.append(f"{m}x{n} ({dt:.1f}s)")
         if t_ns + t_rw >= budget_s:
             break
+    # the scaling check on the largest shape (by NS5 FLOPs and by elements)
+    lm, ln = largest
+    big_rw = max(distinct, key=lambda s: s[0] * s[1])
+    pred_ns = t_ns / ns_flops * po.ns5_flops(lm, ln) if ns_flops else None
+    pred_rw = t_rw / rw_elems * big_rw[0] * big_rw[1]
+    meas_ns = whole(lm, ln, 0)
+    meas_rw = whole(big_rw[0], big_rw[1], 1)
+    t_ns += meas_ns
+    ns_flops += po.ns5_flops(lm, ln)
+    ns_desc.append(f"{lm}x{ln} ({meas_ns:.1f}s)")
+    t_rw += meas_rw
+    rw_elems += big_rw[0] * big_rw[1]
+    rw_desc.append(f"{big_rw[0]}x{big_rw[1]} whole")
     total_flops = sum(po.ns5_flops(m, n) for m, n in shapes)
     total_elems = sum(m * n for m, n in shapes)
     T_ref = t_ns / ns_flops * total_flops * 1e3
@@ -237,10 +279,16 @@ def cpu_baseline(wl_idx, wl, K, cfg_vals, budget_s: float = 12.0):
         "value": amort, "unit": "ms", "cores": int(threads), "kind": "oracle",
         "host_cpus": os.cpu_count(),
         "refresh_ms": T_ref, "rowwise_ms": T_rw, "sample_seconds": t_ns + t_rw,
+        "scaling_check": {
+            "refresh_shape": f"{lm}x{ln}", "refresh_measured_s": meas_ns, "refresh_predicted_s": pred_ns,
+            "refresh_measured_over_predicted": meas_ns / pred_ns if pred_ns else None,
+            "rowwise_shape": f"{big_rw[0]}x{big_rw[1]}", "rowwise_measured_s": meas_rw,
+            "rowwise_predicted_s": pred_rw, "rowwise_measured_over_predicted": meas_rw / pred_rw,
+        },
         "sample": (f"fp64 NumPy oracle: refresh steps of whole matrices {', '.join(ns_desc)} scaled by NS5 "
-                   f"FLOPs (x{total_flops / ns_flops:.1f}); row-wise steps of 256 full oriented rows of "
-                   f"{', '.join(rw_desc)} ({t_rw:.2f}s) scaled by elements (x{total_elems / rw_elems:.1f}); "
-                   f"amortized over K={K}"),
+                   f"FLOPs (x{total_flops / ns_flops:.1f}); row-wise steps of {', '.join(rw_desc)} "
+                   f"({t_rw:.2f}s) scaled by elements (x{total_elems / rw_elems:.1f}); amortized over K={K}; "
+                   f"linear scaling checked on the largest shapes (scaling_check)"),
     }
 
 
@@ -280,7 +328,7 @@ def main():
     log(f"[bench] workload {wl.name}: {len(shapes)} matrices, "
         f"{sum(m * n for m, n in shapes) / 1e9:.3f} G elements, K={K}, steps={steps}, warmup={warmup}")
     W, M, G = make_inputs(args.config, wl, dev)
-    log(f"[bench] inputs ready; workspace {prm.workspace_bytes(shapes, cfg) / 2**30:.1f} GiB")
+    log(f"[bench] inputs ready; workspace {prm.plan_workspace_bytes(shapes, cfg) / 2**30:.1f} GiB")
 
     stream = torch.cuda.current_stream()
     opt = prm.Optimizer(shapes, cfg, stream=stream.cuda_stream)
@@ -321,10 +369,18 @@ def main():
     elems = sum(m * n for m, n in shapes)
     rw_bytes = elems * (gb + 4 + 4 + 2 * wb)
     ns_flops = sum(po.ns5_flops(m, n) for m, n in shapes)
-    refresh_mfma_frac = ns_flops / (T_ref * 1e-3) / (PEAK_BF16_TFLOPS * 1e12) if ref else None
+    exec_flops = executed_ns5_flops(shapes)
+    ns_exec = sum(exec_flops.values())
+    # two readings of "MFMA %" of the refresh step: the paper's algorithmic
+    # FLOPs over the whole step time (what a dense GEMM chain would need), and
+    # the FLOPs the kernels actually issue (the symmetric products compute
+    # only upper tiles, so this is the utilisation of the matrix cores)
+    refresh_alg_frac = ns_flops / (T_ref * 1e-3) / (PEAK_BF16_TFLOPS * 1e12) if ref else None
+    refresh_exec_frac = ns_exec / (T_ref * 1e-3) / (PEAK_BF16_TFLOPS * 1e12) if ref else None
     rowwise_hbm_frac = rw_bytes / (T_rw * 1e-3) / (PEAK_HBM_GBS * 1e9) if rw else None
 
     kernels, roofline, roofline_rw = None, None, None
+    gemm_exec_frac = None
     if not args.no_profile:
         while t % K != 0:
             t += 1
@@ -354,6 +410,17 @@ def main():
                     "alg_per_launch": k["alg_bytes"] / k["launches"]}
 
         roofline = roof(dom, kd)
+        # executed MFMA rate of each GEMM kind over its own launches (per refresh
+        # step: the profiled period holds one refresh)
+        gemm_exec_frac = {}
+        for kname, fl in exec_flops.items():
+            k = kernels[kname]
+            if k["launches"] and k["total_ms"] > 0:
+                gemm_exec_frac[kname] = fl / (k["total_ms"] * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
+        if roofline is not None and roofline["kernel"] in exec_flops:
+            roofline["executed_per_launch"] = exec_flops[roofline["kernel"]] / roofline["launches"]
+            roofline["executed_frac"] = roofline["executed_per_launch"] / (roofline["mean_launch_ms"] * 1e-3) / (
+                PEAK_BF16_TFLOPS * 1e12)
         rw_names = [k for k in ("rw_wide", "rw_generic", "rw_tall_stats", "rw_tall_apply") if kernels[k]["launches"]]
         if rw_names:
             dom_rw = max(rw_names, key=lambda k: kernels[k]["total_ms"])
@@ -436,11 +503,16 @@ def main():
                    "parallelism": "single GPU", "variants": args.variant},
         "refresh_ms": T_ref,
         "rowwise_ms": T_rw,
-        "refresh_mfma_frac": refresh_mfma_frac,
+        "refresh_alg_tflops_frac": refresh_alg_frac,
+        "refresh_executed_mfma_frac": refresh_exec_frac,
+        "refresh_executed_tflop": ns_exec / 1e12,
+        "gemm_executed_mfma_frac": gemm_exec_frac,
         "rowwise_hbm_frac": rowwise_hbm_frac,
         "peaks_measured": peaks,
-        "refresh_mfma_frac_of_measured": (ns_flops / (T_ref * 1e-3) / (peaks["mfma_bf16_tflops"] * 1e12)
-                                          if ref and peaks else None),
+        "refresh_alg_tflops_frac_of_measured": (ns_flops / (T_ref * 1e-3) / (peaks["mfma_bf16_tflops"] * 1e12)
+                                                if ref and peaks else None),
+        "refresh_executed_mfma_frac_of_measured": (ns_exec / (T_ref * 1e-3) / (peaks["mfma_bf16_tflops"] * 1e12)
+                                                   if ref and peaks else None),
         "rowwise_hbm_frac_of_measured": (rw_bytes / (T_rw * 1e-3) / (peaks["hbm_rowwise_mix_gbs"] * 1e9)
                                          if rw and peaks else None),
         "amortized_ms_by_K": ({str(k): (T_ref + (k - 1) * T_rw) / k for k in (1, 3, 5, 10)}

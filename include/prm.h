@@ -63,7 +63,7 @@ extern "C" {
 typedef enum prm_dtype { PRM_F32 = 0, PRM_BF16 = 1 } prm_dtype;
 
 /* Shape scale s(W) of eq. (periodic-direction); the paper names it a
- * "shape-dependent update scale" without a formula. */
+ * scale that depends on the matrix shape, without a formula. */
 typedef enum prm_scale_mode {
   PRM_SCALE_ONE = 0,          /* s = 1 */
   PRM_SCALE_SQRT_ASPECT = 1,  /* s = sqrt(max(1, m/n)) (default) */
@@ -77,7 +77,8 @@ typedef struct prm_config {
   float wd;              /* decoupled weight decay lambda, >= 0 */
   float gamma;           /* RowNorm multiplier (> 0); scales only the RowNorm branch */
   float eps_rownorm;     /* RowNorm clamp, > 0 (applied after the square root) */
-  float eps_ns;          /* NS input normalization X0 = U/(||U||_F + eps_ns), >= 0 */
+  float eps_ns;          /* NS input normalization X0 = U/(||U||_F + eps_ns), > 0
+                            (a zero momentum then gives a zero direction) */
   float ns_a, ns_b, ns_c;/* quintic coefficients (3.4445, -4.7750, 2.0315) */
   int32_t nesterov;      /* 0: U = M;  1: U = G + beta*M (after the momentum update) */
   int32_t ema_dampening; /* 0: M = beta*M + G;  1: M = beta*M + (1-beta)*G */
@@ -99,15 +100,22 @@ typedef struct prm_ctx prm_ctx; /* opaque */
 void prm_config_default(prm_config* cfg);
 
 /* Create a context for n_mats matrices of shapes rows[i] x cols[i] (host
- * arrays, each in [1, 2^24]; n_mats >= 0).  Validates cfg, groups the matrices by
- * oriented NS5 shape, plans and allocates the device workspace (hipMalloc on
- * the current device) and records `hip_stream` for later calls.
- * On success *out owns the workspace until prm_destroy. */
+ * arrays, each in [1, 2^24]; n_mats >= 0): the fixed set W_M of 2-D weight
+ * matrices that Alg. 1 loops over, with the hyperparameters of eq.
+ * (periodic-direction) in cfg (K, beta, lr, wd, gamma, ...).  Validates cfg,
+ * groups the matrices by oriented NS5 shape, plans and allocates the device
+ * workspace (hipMalloc on the current device) and records `hip_stream` for
+ * later calls.  On success *out owns the workspace until prm_destroy.
+ * Errors: PRM_EINVAL / PRM_EDTYPE for a bad cfg or shape, PRM_ENOMEM when the
+ * workspace does not fit, PRM_EHIP for a failed HIP call; *out is then NULL
+ * and nothing stays allocated. */
 int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* cols,
              const prm_config* cfg, void* hip_stream);
 
-/* One optimizer step t (0-based, >= 0) over every matrix, enqueued on the
- * context's stream.  params[i]: W (param_dtype), grads[i]: G (grad_dtype),
+/* One optimizer step t (0-based, >= 0) over every matrix: the body of the
+ * loop over t in Alg. 1 (momentum update, rho_t of eq. periodic-direction,
+ * NS5 refresh or gamma RowNorm, shape scale, decoupled weight decay and the
+ * parameter write), enqueued on the context's stream.  params[i]: W (param_dtype), grads[i]: G (grad_dtype),
  * momentum[i]: M (fp32); all device pointers, 16-byte aligned.  lr < 0 uses
  * cfg->lr.  *did_refresh (nullable) receives rho_t, computed on the host.
  * Runs on the device the context was created on; the caller's current device
@@ -115,21 +123,34 @@ int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* 
 int prm_step(prm_ctx* ctx, void* const* params, const void* const* grads,
              float* const* momentum, int64_t step, float lr, int32_t* did_refresh);
 
-/* prm_step that also writes D = s(W) * O^{-1}(D~) (fp32, m x n, row-major,
- * device) into direction_out[i] for every matrix whose entry is not NULL
- * (NULL: that matrix's direction is not written).  Parity checking only. */
+/* prm_step that also writes the direction D = s(W) * O^{-1}(D~) of eq.
+ * (periodic-direction) (fp32, m x n, row-major, device, caller-owned) into
+ * direction_out[i] for every matrix whose entry is not NULL (NULL: that
+ * matrix's direction is not written).  W and M end bitwise as with prm_step.
+ * Parity checking only. */
 int prm_step_debug(prm_ctx* ctx, void* const* params, const void* const* grads,
                    float* const* momentum, int64_t step, float lr, int32_t* did_refresh,
                    float* const* direction_out);
 
-/* rho_t = 1[t mod K = 0] (Sec. 3.3): 1 or 0, or PRM_EINVAL for K < 1 or t < 0.
- * Pure host function. */
-int prm_is_refresh(int64_t step, int32_t K);
+/* The refresh indicator rho_t of the context's schedule (Sec. 3.3, eq.
+ * periodic-direction; Alg. 1): 1[t mod K = 0] for 0-based t, or 0 for every t
+ * with cfg.never_refresh.  Returns 1 or 0 (what prm_step would report in
+ * *did_refresh), or PRM_EINVAL for a NULL ctx or t < 0.  Host only. */
+int prm_is_refresh(const prm_ctx* ctx, int64_t step);
 
-/* Device bytes prm_init would allocate for these shapes and cfg (pure host
- * planning, no device call). */
-int prm_workspace_bytes(int32_t n_mats, const int64_t* rows, const int64_t* cols,
-                        const prm_config* cfg, uint64_t* out_bytes);
+/* Device bytes the context holds for the step of Alg. 1 (NS5 workspace,
+ * tall-matrix statistics of eq. sharded-tall-rownorm and small per-matrix
+ * scalars; not the descriptor and work-list tables) in *out_bytes.
+ * PRM_EINVAL for a NULL argument.  Host only. */
+int prm_workspace_bytes(const prm_ctx* ctx, size_t* out_bytes);
+
+/* The same two quantities without a context, for planning: rho_t =
+ * 1[t mod K = 0] (PRM_EINVAL for K < 1 or t < 0), and the device bytes
+ * prm_init would allocate for these shapes and cfg (same validation and error
+ * codes as prm_init; no device call). */
+int prm_schedule_is_refresh(int64_t step, int32_t K);
+int prm_plan_workspace_bytes(int32_t n_mats, const int64_t* rows, const int64_t* cols,
+                             const prm_config* cfg, uint64_t* out_bytes);
 
 /* Per-kernel-class timing on the context's stream, for measurement.
  * prm_profile_enable(ctx, 1) makes later steps record a HIP event pair around

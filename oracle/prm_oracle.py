@@ -23,13 +23,15 @@ reason, in the design notes of the repository):
 
 * momentum update   M <- beta*M + G (heavy-ball); optional dampening
                     M <- beta*M + (1-beta)*G and optional Nesterov input
-                    U = G + beta*M.  Alg. 1 only says "as in Section 2", which
-                    never writes the formula; beta = 0.95 (hyperparameter table).
-* NS input scaling  X0 = M~ / (||M~||_F + eps_ns), eps_ns = 1e-7 (App. "Per-matrix
+                    U = G + beta*M.  Alg. 1 defers the momentum update to Sec. 2,
+                    which never writes it out; beta = 0.95 (hyperparameter table).
+* NS input scaling  X0 = M~ / (||M~||_F + eps_ns), eps_ns = 1e-7 > 0 (App. "Per-matrix
                     arithmetic" names an input normalization without its form).
+* ablations         Table 3a: RowNorm on every step (never_refresh) and the
+                    scalar-controlled variant (gamma on both branches).
 * eps of RowNorm    1e-8 (the only epsilon the paper prints).
-* shape scale s(W)  sqrt(max(1, m/n)) by default (the paper names a
-                    "shape-dependent update scale" without a formula).
+* shape scale s(W)  sqrt(max(1, m/n)) by default (the paper scales the update
+                    by a factor that depends on the shape, without a formula).
                     PARITY UNPINNED BY THE PAPER: s(W) is a convention that
                     both sides read from the same configuration; the tests pin
                     only its stated definition (update RMS = 1/sqrt(n) for an
@@ -99,7 +101,7 @@ def orient_inv(Xt: np.ndarray, m: int, n: int) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------
-# momentum (reading of Alg. 1 "update every momentum as in Section 2")
+# momentum (a reading: Alg. 1 refers the momentum update to Sec. 2)
 # --------------------------------------------------------------------------
 def momentum_update(M: np.ndarray, G: np.ndarray, beta: float,
                     dampening: bool = False) -> np.ndarray:
@@ -240,6 +242,12 @@ class PRMConfig:
     never_refresh: bool = False     # ablation: RowNorm at every step
     gamma_on_refresh: bool = False  # ablation: scalar-controlled (gamma on both branches)
     coeffs: tuple = field(default=NS_COEFFS)
+
+    def __post_init__(self):
+        # both clamps must be positive: a zero momentum (or a zero row) then
+        # gives a zero direction instead of 0/0
+        if self.K < 1 or not self.eps_rownorm > 0 or not self.eps_ns > 0:
+            raise ValueError("need K >= 1, eps_rownorm > 0 and eps_ns > 0")
 
 
 def direction(U: np.ndarray, t: int, cfg: PRMConfig) -> tuple[np.ndarray, int]:

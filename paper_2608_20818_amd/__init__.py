@@ -14,7 +14,7 @@ import os
 __all__ = [
     "PRMError", "Config", "KernelStats", "Optimizer", "AdamWConfig", "AuxAdamW", "load",
     "config_default", "adamw_config_default",
-    "is_refresh", "workspace_bytes", "PRM_OK", "PRM_EINVAL", "PRM_EDTYPE", "PRM_EALIGN",
+    "schedule_is_refresh", "plan_workspace_bytes", "PRM_OK", "PRM_EINVAL", "PRM_EDTYPE", "PRM_EALIGN",
     "PRM_ENOMEM", "PRM_EHIP", "F32", "BF16", "KERNEL_CLASSES",
 ]
 
@@ -84,11 +84,15 @@ def load() -> ctypes.CDLL:
     L.prm_step.restype = ctypes.c_int
     L.prm_step_debug.argtypes = step_args + [ctypes.POINTER(P)]
     L.prm_step_debug.restype = ctypes.c_int
-    L.prm_is_refresh.argtypes = [ctypes.c_int64, ctypes.c_int32]
+    L.prm_is_refresh.argtypes = [P, ctypes.c_int64]
     L.prm_is_refresh.restype = ctypes.c_int
-    L.prm_workspace_bytes.argtypes = [ctypes.c_int32, i64p, i64p, ctypes.POINTER(Config),
-                                      ctypes.POINTER(ctypes.c_uint64)]
+    L.prm_workspace_bytes.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
     L.prm_workspace_bytes.restype = ctypes.c_int
+    L.prm_schedule_is_refresh.argtypes = [ctypes.c_int64, ctypes.c_int32]
+    L.prm_schedule_is_refresh.restype = ctypes.c_int
+    L.prm_plan_workspace_bytes.argtypes = [ctypes.c_int32, i64p, i64p, ctypes.POINTER(Config),
+                                           ctypes.POINTER(ctypes.c_uint64)]
+    L.prm_plan_workspace_bytes.restype = ctypes.c_int
     L.prm_profile_enable.argtypes = [P, ctypes.c_int32]
     L.prm_profile_enable.restype = ctypes.c_int
     L.prm_profile_read.argtypes = [P, ctypes.POINTER(KernelStats), ctypes.c_int32]
@@ -131,8 +135,9 @@ def config_default(**overrides) -> Config:
     return cfg
 
 
-def is_refresh(step: int, K: int) -> int:
-    return _check(load().prm_is_refresh(step, K))
+def schedule_is_refresh(step: int, K: int) -> int:
+    """rho_t = 1[t mod K = 0] without a context (prm_schedule_is_refresh)."""
+    return _check(load().prm_schedule_is_refresh(step, K))
 
 
 def _shape_arrays(shapes):
@@ -142,10 +147,11 @@ def _shape_arrays(shapes):
     return n, rows, cols
 
 
-def workspace_bytes(shapes, cfg: Config) -> int:
+def plan_workspace_bytes(shapes, cfg: Config) -> int:
+    """Device bytes prm_init would allocate (prm_plan_workspace_bytes)."""
     n, rows, cols = _shape_arrays(shapes)
     out = ctypes.c_uint64()
-    _check(load().prm_workspace_bytes(n, rows, cols, ctypes.byref(cfg), ctypes.byref(out)))
+    _check(load().prm_plan_workspace_bytes(n, rows, cols, ctypes.byref(cfg), ctypes.byref(out)))
     return out.value
 
 
@@ -230,6 +236,16 @@ class Optimizer:
             D = arr(*[0 if x is None else _ptr(x) for x in directions])
             _check(L.prm_step_debug(self._ctx, P, G, M, int(step), float(lr), ctypes.byref(rho), D))
         return rho.value
+
+    def is_refresh(self, step: int) -> int:
+        """rho_t of this context's schedule (prm_is_refresh)."""
+        return _check(load().prm_is_refresh(self._ctx, int(step)))
+
+    def workspace_bytes(self) -> int:
+        """Device bytes this context holds (prm_workspace_bytes)."""
+        out = ctypes.c_size_t()
+        _check(load().prm_workspace_bytes(self._ctx, ctypes.byref(out)))
+        return out.value
 
     def profile_enable(self, on: bool = True):
         _check(load().prm_profile_enable(self._ctx, 1 if on else 0))

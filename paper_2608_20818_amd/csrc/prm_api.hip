@@ -137,7 +137,7 @@ int validate_cfg(const prm_config* c) {
   if (!(c->gamma > 0.f) || !std::isfinite(c->gamma)) return fail(PRM_EINVAL, "gamma must be > 0");
   if (!(c->eps_rownorm > 0.f) || !std::isfinite(c->eps_rownorm))
     return fail(PRM_EINVAL, "eps_rownorm must be finite and > 0");
-  if (!(c->eps_ns >= 0.f) || !std::isfinite(c->eps_ns)) return fail(PRM_EINVAL, "eps_ns must be finite and >= 0");
+  if (!(c->eps_ns > 0.f) || !std::isfinite(c->eps_ns)) return fail(PRM_EINVAL, "eps_ns must be finite and > 0");
   if (!std::isfinite(c->ns_a) || !std::isfinite(c->ns_b) || !std::isfinite(c->ns_c))
     return fail(PRM_EINVAL, "NS coefficients must be finite");
   if (c->nesterov != 0 && c->nesterov != 1) return fail(PRM_EINVAL, "nesterov must be 0 or 1");
@@ -586,6 +586,11 @@ int refresh_step(prm_ctx* c, float lr, bool debug) {
   return PRM_OK;
 }
 
+// rho_t of eq. (periodic-direction) for a validated configuration and t >= 0.
+int refresh_of(const prm_config& cfg, int64_t t) {
+  return cfg.never_refresh ? 0 : (t % cfg.K == 0 ? 1 : 0);
+}
+
 int do_step(prm_ctx* c, void* const* params, const void* const* grads, float* const* momentum,
             int64_t t, float lr, int32_t* did_refresh, float* const* dirs, bool debug) {
   if (!c) return fail(PRM_EINVAL, "ctx is NULL");
@@ -608,7 +613,7 @@ int do_step(prm_ctx* c, void* const* params, const void* const* grads, float* co
       }
     }
   }
-  const int rho = c->cfg.never_refresh ? 0 : (t % c->cfg.K == 0 ? 1 : 0);
+  const int rho = refresh_of(c->cfg, t);
   if (did_refresh) *did_refresh = rho;
   if (n == 0) return PRM_OK;
   DeviceScope dev;
@@ -675,14 +680,26 @@ void prm_config_default(prm_config* cfg) {
   cfg->grad_dtype = PRM_BF16;
 }
 
-int prm_is_refresh(int64_t step, int32_t K) {
+int prm_schedule_is_refresh(int64_t step, int32_t K) {
   if (K < 1) return fail(PRM_EINVAL, "K must be >= 1 (got %d)", K);
   if (step < 0) return fail(PRM_EINVAL, "step must be >= 0 (got %lld)", (long long)step);
   return step % K == 0 ? 1 : 0;
 }
 
-int prm_workspace_bytes(int32_t n_mats, const int64_t* rows, const int64_t* cols,
-                        const prm_config* cfg, uint64_t* out_bytes) {
+int prm_is_refresh(const prm_ctx* ctx, int64_t step) {
+  if (!ctx) return fail(PRM_EINVAL, "ctx is NULL");
+  if (step < 0) return fail(PRM_EINVAL, "step must be >= 0 (got %lld)", (long long)step);
+  return refresh_of(ctx->cfg, step);
+}
+
+int prm_workspace_bytes(const prm_ctx* ctx, size_t* out_bytes) {
+  if (!ctx || !out_bytes) return fail(PRM_EINVAL, "ctx and out_bytes must not be NULL");
+  *out_bytes = (size_t)ctx->plan.total_bytes;
+  return PRM_OK;
+}
+
+int prm_plan_workspace_bytes(int32_t n_mats, const int64_t* rows, const int64_t* cols,
+                             const prm_config* cfg, uint64_t* out_bytes) {
   if (!out_bytes) return fail(PRM_EINVAL, "out_bytes is NULL");
   Plan P;
   int rc = make_plan(n_mats, rows, cols, cfg, P);

@@ -261,7 +261,7 @@ __global__ __launch_bounds__(256) void rw_tall_stats_scalar_kernel(const MatDesc
 }
 
 // Column norms of a tall matrix: fixed-order sum over row blocks, square root,
-// then the clamp (Alg. 2: take the square root and then clamp_min(eps)).
+// then the clamp at eps (Alg. 2, row-wise branch: the clamp follows the square root).
 __global__ __launch_bounds__(256) void rw_tall_finalize_kernel(const MatDesc* __restrict__ md,
                                                                const Item* __restrict__ items,
                                                                RwParams p) {

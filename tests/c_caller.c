@@ -13,8 +13,9 @@
  *   G<i>_<s>.bin  gradient of step s = 0 .. steps-1 (grad_dtype)
  * runs steps t0 .. t0 + steps - 1 through prm_step_debug on one stream, and
  * writes W<i>.out, M<i>.out (after the last step), D<i>.out (the direction of
- * the last step, fp32) and rho.txt (rho_t of every step, from the library and
- * from prm_is_refresh).  Returns 0, or -1 with a message in `msg`.
+ * the last step, fp32) and rho.txt (rho_t of every step: from prm_step_debug,
+ * from prm_is_refresh on the context and from prm_schedule_is_refresh).
+ * Returns 0, or -1 with a message in `msg`.
  */
 #include <stdarg.h>
 #include <stdint.h>
@@ -182,7 +183,7 @@ int prm_c_run_case(const char* dir, char* msg, int msglen) {
       rc = failf(&e, "prm_step_debug(t=%lld): %s", t, prm_last_error());
       break;
     }
-    fprintf(rf, "%lld %d %d\n", t, rho, prm_is_refresh(t, K));
+    fprintf(rf, "%lld %d %d %d\n", t, rho, prm_is_refresh(ctx, t), prm_schedule_is_refresh(t, K));
   }
   if (rf) fclose(rf);
   if (rc == 0 && hipStreamSynchronize(stream) != hipSuccess) rc = failf(&e, "hipStreamSynchronize failed");

@@ -27,7 +27,8 @@ def test_library_exports_every_declared_symbol():
     lib = prm.load()
     names = declared_functions()
     assert {"prm_init", "prm_step", "prm_step_debug", "prm_is_refresh", "prm_workspace_bytes",
-            "prm_destroy", "prm_last_error", "prm_config_default"} <= set(names)
+            "prm_destroy", "prm_last_error", "prm_config_default", "prm_schedule_is_refresh",
+            "prm_plan_workspace_bytes"} <= set(names)
     out = subprocess.run(["nm", "-D", "--defined-only", prm.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r" T (prm_\w+)", out))
@@ -51,46 +52,79 @@ def test_config_defaults_are_paper_values():
     assert cfg.param_dtype == prm.BF16 and cfg.grad_dtype == prm.BF16
 
 
+def _prototypes():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return {m.group(1): re.sub(r"\s+", " ", m.group(0)) for m in re.finditer(r"\bint (prm_\w+)\([^;]*\);", text)}
+
+
+def test_boundary_signatures_follow_the_scope_table():
+    # the context-taking schedule and workspace queries of the boundary, and
+    # the context-free planners beside them
+    p = _prototypes()
+    assert p["prm_is_refresh"] == "int prm_is_refresh(const prm_ctx* ctx, int64_t step);"
+    assert p["prm_workspace_bytes"] == "int prm_workspace_bytes(const prm_ctx* ctx, size_t* out_bytes);"
+    assert p["prm_schedule_is_refresh"] == "int prm_schedule_is_refresh(int64_t step, int32_t K);"
+    assert p["prm_init"].startswith("int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, "
+                                    "const int64_t* cols, const prm_config* cfg, void* hip_stream)")
+    assert p["prm_step"].startswith("int prm_step(prm_ctx* ctx, void* const* params, const void* const* grads, "
+                                    "float* const* momentum, int64_t step, float lr, int32_t* did_refresh)")
+    assert p["prm_destroy"] == "int prm_destroy(prm_ctx* ctx);"
+    L = prm.load()
+    out = ctypes.c_size_t(7)
+    assert L.prm_is_refresh(None, 0) == prm.PRM_EINVAL
+    assert L.prm_workspace_bytes(None, ctypes.byref(out)) == prm.PRM_EINVAL and out.value == 7
+    assert L.prm_last_error().decode() != ""
+
+
+def test_declarations_cite_the_paper():
+    # every step entry point names the passage that defines it
+    text = open(HEADER).read()
+    for name in ("prm_init", "prm_step", "prm_step_debug", "prm_is_refresh", "prm_workspace_bytes"):
+        i = text.index(f"int {name}(")
+        comment = re.sub(r"\s+\*?\s*", " ", text[text.rindex("/*", 0, i):i])
+        assert re.search(r"Alg\. 1|eq\. \(?periodic-direction|Sec\. 3\.3", comment), name
+
+
 @pytest.mark.parametrize("K", [1, 2, 3, 4, 5, 7, 10, 12])
 def test_is_refresh_matches_oracle_exhaustively(K):
     for t in range(0, 600):
-        assert prm.is_refresh(t, K) == po.refresh_indicator(t, K)
+        assert prm.schedule_is_refresh(t, K) == po.refresh_indicator(t, K)
     for t in (2 ** 40, 2 ** 40 + 1, 2 ** 62):
-        assert prm.is_refresh(t, K) == po.refresh_indicator(t, K)
+        assert prm.schedule_is_refresh(t, K) == po.refresh_indicator(t, K)
 
 
 def test_is_refresh_rejects_bad_args():
     with pytest.raises(prm.PRMError) as e:
-        prm.is_refresh(0, 0)
+        prm.schedule_is_refresh(0, 0)
     assert e.value.code == prm.PRM_EINVAL
     with pytest.raises(prm.PRMError):
-        prm.is_refresh(-1, 3)
+        prm.schedule_is_refresh(-1, 3)
 
 
 def test_workspace_planning():
     cfg = prm.config_default()
     tiny = synth.WORKLOADS[0].shapes
-    b = prm.workspace_bytes(tiny, cfg)
+    b = prm.plan_workspace_bytes(tiny, cfg)
     assert b > 0
     # NS5 region of one matrix: 4 rp cp + 4 rp^2 + 8 rp bytes (the transposed
     # iterate and the next one in bf16, off-diagonal A and B in bf16, their
     # diagonals in fp32)
-    one = prm.workspace_bytes([(256, 1024)], cfg)
+    one = prm.plan_workspace_bytes([(256, 1024)], cfg)
     assert one >= 4 * 256 * 1024 + 4 * 256 * 256 + 8 * 256
     # a budget smaller than one matrix is refused; a small budget forces chunking
     small = prm.config_default(workspace_budget_bytes=1000)
     with pytest.raises(prm.PRMError) as e:
-        prm.workspace_bytes(tiny, small)
+        prm.plan_workspace_bytes(tiny, small)
     assert e.value.code == prm.PRM_ENOMEM
     chunked = prm.config_default(workspace_budget_bytes=8 * 256 * 1024 + 6 * 256 * 256 + 4096)
-    assert prm.workspace_bytes(tiny, chunked) < b
-    assert prm.workspace_bytes([], cfg) == 0
+    assert prm.plan_workspace_bytes(tiny, chunked) < b
+    assert prm.plan_workspace_bytes([], cfg) == 0
 
 
 def test_workspace_fits_dit_configs():
     cfg = prm.config_default()
     for wl in synth.WORKLOADS[1:]:
-        ws = prm.workspace_bytes(wl.shapes, cfg)
+        ws = prm.plan_workspace_bytes(wl.shapes, cfg)
         state = sum(m * n for m, n in wl.shapes) * (2 + 2 + 4)
         assert ws <= (32 << 30) + (1 << 30)
         assert state + ws < 288e9 * 0.95, wl.name
@@ -101,6 +135,7 @@ def test_workspace_fits_dit_configs():
     ("gamma", 0.0, prm.PRM_EINVAL), ("eps_rownorm", 0.0, prm.PRM_EINVAL),
     ("lr", -1.0, prm.PRM_EINVAL), ("wd", -0.5, prm.PRM_EINVAL), ("scale_mode", 7, prm.PRM_EINVAL),
     ("eps_rownorm", float("inf"), prm.PRM_EINVAL), ("eps_ns", float("nan"), prm.PRM_EINVAL),
+    ("eps_ns", 0.0, prm.PRM_EINVAL), ("eps_ns", -1e-7, prm.PRM_EINVAL),
     ("param_dtype", 5, prm.PRM_EDTYPE), ("grad_dtype", -1, prm.PRM_EDTYPE),
     ("nesterov", 2, prm.PRM_EINVAL),
 ])
@@ -123,9 +158,9 @@ def test_bad_shapes_rejected():
         rows = (ctypes.c_int64 * 1)(r)
         cols = (ctypes.c_int64 * 1)(c)
         out = ctypes.c_uint64()
-        assert L.prm_workspace_bytes(1, rows, cols, ctypes.byref(cfg), ctypes.byref(out)) == prm.PRM_EINVAL
-    assert L.prm_workspace_bytes(-1, None, None, ctypes.byref(cfg), ctypes.byref(ctypes.c_uint64())) == prm.PRM_EINVAL
-    assert L.prm_workspace_bytes(2, None, None, ctypes.byref(cfg), ctypes.byref(ctypes.c_uint64())) == prm.PRM_EINVAL
+        assert L.prm_plan_workspace_bytes(1, rows, cols, ctypes.byref(cfg), ctypes.byref(out)) == prm.PRM_EINVAL
+    assert L.prm_plan_workspace_bytes(-1, None, None, ctypes.byref(cfg), ctypes.byref(ctypes.c_uint64())) == prm.PRM_EINVAL
+    assert L.prm_plan_workspace_bytes(2, None, None, ctypes.byref(cfg), ctypes.byref(ctypes.c_uint64())) == prm.PRM_EINVAL
 
 
 def test_null_context_calls_fail_cleanly():

@@ -85,7 +85,7 @@ def test_c_caller_tiny_trajectory(tmp_path):
     wbudget = np.zeros(len(shapes))
     for t in range(steps):
         Wo, Mo, Do, rho_o = po.step(Wo, Mo, [g[t] for _, _, g in inputs], t, oc)
-        assert rho[t] == (t, rho_o, rho_o), rho[t]
+        assert rho[t] == (t, rho_o, rho_o, rho_o), rho[t]
         tol = pc.TOL_NS5 if rho_o else pc.TOL_ROWWISE
         # each step moves W by eta D; the GPU direction is within tol of the oracle's
         wbudget += [pc.f32(cfg.lr) * tol * np.linalg.norm(d) * 1.01 for d in Do]
@@ -109,7 +109,7 @@ def test_c_caller_bf16_one_step(tmp_path, t0):
     oc = pc.oracle_config(cfg)
     for i, (w0, m0, g) in enumerate(inputs):
         Wo, Mo, Do, rho_o = po.step_matrix(w0, m0, g[t0], t0, oc)
-        assert rho == [(t0, rho_o, rho_o)]
+        assert rho == [(t0, rho_o, rho_o, rho_o)]
         tol = pc.TOL_NS5 if rho_o else pc.TOL_ROWWISE
         r = out[i]
         eD = pc.rel(r["D"], Do)

@@ -103,9 +103,9 @@ def test_variants(flag, t):
 def test_several_workspace_chunks():
     shapes = [(256, 512), (512, 256), (128, 640), (200, 200), (256, 512)]
     # a budget that holds the largest single matrix but not all of them
-    one = max(prm.workspace_bytes([s], prm.config_default()) for s in shapes)
+    one = max(prm.plan_workspace_bytes([s], prm.config_default()) for s in shapes)
     cfg = prm.config_default(K=2, lr=0.01, wd=0.01, workspace_budget_bytes=one)
-    assert prm.workspace_bytes(shapes, cfg) < prm.workspace_bytes(shapes, prm.config_default())
+    assert prm.plan_workspace_bytes(shapes, cfg) < prm.plan_workspace_bytes(shapes, prm.config_default())
     rho, res = run_one_step(shapes, cfg, 0, workload_id=92)
     check(res, rho, cfg, shapes, cfg.lr)
 
@@ -323,3 +323,30 @@ def test_largest_dimension(t):
     assert rho == (1 if t == 0 else 0)
     check(res, rho, cfg, shapes, cfg.lr)
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("flag", [None, "never_refresh"])
+def test_context_schedule_and_workspace_queries(flag):
+    # prm_is_refresh on a context reports what prm_step returns in did_refresh
+    # (the schedule of eq. periodic-direction, or none for the RowNorm-every-step
+    # ablation); prm_workspace_bytes reports what the planner said prm_init
+    # would allocate
+    shapes = [(96, 320), (300, 88)]
+    kw = {flag: 1} if flag else {}
+    cfg = prm.config_default(K=3, param_dtype=0, grad_dtype=0, **kw)
+    inputs = pc.host_inputs(shapes, cfg, 94, steps=tuple(range(7)))
+    W = [pc.to_device(w, 0) for w, _, _ in inputs]
+    M = [pc.to_device(m, 0) for _, m, _ in inputs]
+    oc = pc.oracle_config(cfg)
+    with prm.Optimizer(shapes, cfg) as opt:
+        assert opt.workspace_bytes() == prm.plan_workspace_bytes(shapes, cfg)
+        for t in range(7):
+            G = [pc.to_device(g[t], 0) for _, _, g in inputs]
+            want = 0 if flag else po.refresh_indicator(t, cfg.K)
+            assert opt.is_refresh(t) == want
+            assert opt.step(W, G, M, t) == want
+        for t in (2 ** 40, 2 ** 40 + 1):
+            assert opt.is_refresh(t) == (0 if flag else po.refresh_indicator(t, cfg.K))
+        with pytest.raises(prm.PRMError):
+            opt.is_refresh(-1)
+        torch.cuda.synchronize()

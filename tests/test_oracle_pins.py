@@ -98,12 +98,95 @@ def test_momentum_closed_form_after_three_steps():
                                rtol=1e-13, atol=1e-14)
 
 
-def test_nesterov_input():
+def _quintic5(y):
+    """phi5 by a plain scalar loop over the paper's printed coefficients."""
+    a, b, c = GOLD["ns_coefficients"]["value"]
+    for _ in range(5):
+        y = a * y + b * y ** 3 + c * y ** 5
+    return y
+
+
+def _unit_rows(E):
+    return E / np.linalg.norm(E, axis=1, keepdims=True)
+
+
+def pin_nesterov_zero_momentum():
+    """With M_0 = 0 the Nesterov input is G + beta * G = (1 + beta) G, a positive
+    multiple of the plain input M_1 = G; both direction maps are positively
+    homogeneous, so every direction must equal the non-Nesterov one."""
     rng = np.random.default_rng(2)
-    M = rng.standard_normal((4, 6))
-    G = rng.standard_normal((4, 6))
-    np.testing.assert_array_equal(po.momentum_direction_input(M, G, 0.9, False), M)
-    np.testing.assert_allclose(po.momentum_direction_input(M, G, 0.9, True), G + 0.9 * M)
+    for (m, n) in [(6, 14), (14, 6)]:
+        W = rng.standard_normal((m, n))
+        G = rng.standard_normal((m, n))
+        for t in (0, 1):
+            c0 = po.PRMConfig(K=2, beta=0.9)
+            c1 = po.PRMConfig(K=2, beta=0.9, nesterov=True)
+            _, M0, D0, _ = po.step_matrix(W, np.zeros((m, n)), G, t, c0)
+            _, M1, D1, _ = po.step_matrix(W, np.zeros((m, n)), G, t, c1)
+            np.testing.assert_array_equal(M1, M0)          # the state does not see Nesterov
+            assert rel(D1, D0) < 1e-6, (m, n, t)
+
+
+def pin_nesterov_lookahead():
+    """Nesterov as a look-ahead: since M_t = beta M_{t-1} + G_t, the input
+    G_t + beta M_t equals the extrapolation M_t + beta (M_t - M_{t-1}).  Over a
+    trajectory, every Nesterov direction must be the direction of that
+    extrapolation of the momenta the (separately pinned) momentum recursion
+    produced: through the SVD closed form on refresh steps, rows scaled to unit
+    norm on row-wise steps."""
+    rng = np.random.default_rng(21)
+    beta = 0.9
+    for (m, n) in [(8, 20), (20, 8)]:
+        cfg = po.PRMConfig(K=3, beta=beta, nesterov=True, lr=0.01)
+        W = rng.standard_normal((m, n))
+        M = rng.standard_normal((m, n))
+        s = po.shape_scale(m, n)
+        for t in range(6):
+            G = rng.standard_normal((m, n))
+            W, M_new, D, rho = po.step_matrix(W, M, G, t, cfg)
+            E = po.orient(M_new + beta * (M_new - M))
+            if rho:
+                want = s * po.orient_inv(po.ns5_closed_form(E, cfg.eps_ns), m, n)
+            else:
+                want = s * po.orient_inv(cfg.gamma * _unit_rows(E), m, n)
+            assert rel(D, want) < 1e-11, (m, n, t, rel(D, want))
+            M = M_new
+
+
+def pin_nesterov_constructed_target():
+    """Choose the Nesterov input: for a target U* = sigma u v^T and any M_0, the
+    gradient G = (U* - beta^2 M_0) / (1 + beta) makes G + beta (beta M_0 + G) = U*.
+    A rank-one input has closed-form directions: phi5 of its normalized single
+    singular value times u v^T (refresh), and sign(u_i) v / ||v|| per stored row
+    of a wide matrix (row-wise)."""
+    rng = np.random.default_rng(22)
+    beta, gamma = 0.8, 0.3
+    m, n = 7, 12
+    u, v = rng.standard_normal(m), rng.standard_normal(n)
+    Ustar = 1.7 * np.outer(u, v)
+    M0 = rng.standard_normal((m, n))
+    G = (Ustar - beta ** 2 * M0) / (1 + beta)
+    cfg = po.PRMConfig(K=2, beta=beta, gamma=gamma, nesterov=True)
+    nf = np.linalg.norm(Ustar)
+    y = _quintic5(nf / (nf + cfg.eps_ns))
+    _, _, D, rho = po.step_matrix(np.zeros((m, n)), M0, G, 0, cfg)
+    assert rho == 1
+    assert rel(D, y * np.outer(u / np.linalg.norm(u), v / np.linalg.norm(v))) < 1e-10
+    _, _, D, rho = po.step_matrix(np.zeros((m, n)), M0, G, 1, cfg)
+    assert rho == 0
+    assert rel(D, gamma * np.outer(np.sign(u), v / np.linalg.norm(v))) < 1e-12
+
+
+def test_nesterov_zero_momentum():
+    pin_nesterov_zero_momentum()
+
+
+def test_nesterov_lookahead():
+    pin_nesterov_lookahead()
+
+
+def test_nesterov_constructed_target():
+    pin_nesterov_constructed_target()
 
 
 # ----------------------------------------------------------------- RowNorm
@@ -117,17 +200,21 @@ def test_rownorm_rows_have_unit_norm_and_direction():
     np.testing.assert_allclose(cos, 1.0, rtol=1e-14)
 
 
-def test_rownorm_eps_clamp_after_sqrt():
-    # eq. (rownorm): denominator max(||X_i||, eps).  Zero row -> zero; a row
-    # with norm below eps is divided by eps (not by sqrt(eps) or eps^2).
+def pin_rownorm_eps_clamp_after_sqrt():
+    """eq. (rownorm): denominator max(||X_i||, eps).  A zero row stays zero; a
+    row with norm below eps is divided by eps (not by sqrt(eps) or eps^2)."""
     eps = 1e-2
     X = np.zeros((3, 4))
     X[1] = [3e-3, 4e-3, 0, 0]          # norm 5e-3 < eps
     X[2] = [3.0, 4.0, 0, 0]            # norm 5
     R = po.rownorm(X, eps)
     np.testing.assert_array_equal(R[0], 0.0)
-    np.testing.assert_allclose(R[1], X[1] / eps, rtol=1e-15)
+    np.testing.assert_allclose(R[1], [0.3, 0.4, 0, 0], rtol=1e-14)
     np.testing.assert_allclose(R[2], [0.6, 0.8, 0, 0], rtol=1e-15)
+
+
+def test_rownorm_eps_clamp_after_sqrt():
+    pin_rownorm_eps_clamp_after_sqrt()
 
 
 def test_rownorm_frobenius_and_inner_product_identities():
@@ -162,18 +249,26 @@ def test_rownorm_equivariances():
     np.testing.assert_allclose(po.rownorm(X @ Q, 1e-8), R @ Q, rtol=1e-12, atol=1e-13)
 
 
-def test_sharded_tall_rownorm_equivalence():
-    # Prop. (sharded RowNorm): for tall M, per-shard column sums of squares,
-    # summed, give the dense RowNorm of M^T.
+def pin_sharded_tall_rownorm():
+    """Prop. (sharded RowNorm): for a tall M the oriented rows are the stored
+    columns, and per-shard column sums of squares, summed over any row split,
+    give their norms.  The oracle's step on a tall matrix must produce exactly
+    those column-normalized directions."""
     rng = np.random.default_rng(7)
     M = rng.standard_normal((96, 20))
     eps = 1e-8
-    dense = po.orient_inv(po.rownorm(po.orient(M), eps), 96, 20)
+    cfg = po.PRMConfig(K=2, beta=0.0, gamma=1.0, eps_rownorm=eps, scale_mode=po.SCALE_ONE)
+    _, _, dense, rho = po.step_matrix(np.zeros_like(M), np.zeros_like(M), M, 1, cfg)
+    assert rho == 0
     for p in (1, 2, 3, 7):
         shards = np.array_split(np.arange(96), p)
         q = sum(np.sum(M[s] ** 2, axis=0) for s in shards)
         nu = np.maximum(np.sqrt(q), eps)
-        np.testing.assert_allclose(M / nu[None, :], dense, rtol=1e-13)
+        np.testing.assert_allclose(dense, M / nu[None, :], rtol=1e-13)
+
+
+def test_sharded_tall_rownorm_equivalence():
+    pin_sharded_tall_rownorm()
 
 
 # ----------------------------------------------------------------- NS5
@@ -301,27 +396,28 @@ def test_shape_scale_rms_convention():
 
 
 # ----------------------------------------------------------------- whole step
-def test_step_rank_one_closed_forms():
-    # M0 = 0 and G = sigma u v^T: M1 = G; refresh gives phi5(~1) u v^T (rank one has
-    # a single singular value equal to the Frobenius norm); the row-wise branch
-    # normalizes every oriented row to sign * unit vector.
+def pin_step_rank_one_closed_forms(gamma_on_refresh=False):
+    """M0 = 0 and G = sigma u v^T: M1 = G; a rank-one matrix has one singular
+    value, equal to its Frobenius norm, so refresh gives phi5(~1) u v^T
+    (unit u, v); the row-wise branch maps every oriented row to sign times a
+    unit vector.  With the scalar-controlled ablation (Table 3a: gamma on both
+    branches) the refresh direction is gamma times the plain one and the
+    row-wise one is unchanged."""
     rng = np.random.default_rng(17)
-    a, b, c = GOLD["ns_coefficients"]["value"]
     for (m, n) in [(6, 10), (10, 6)]:
         u = rng.standard_normal(m)
         v = rng.standard_normal(n)
         G = 2.5 * np.outer(u, v)
         W = rng.standard_normal((m, n))
-        cfg = po.PRMConfig(K=2, beta=0.9, gamma=0.3, wd=0.1, lr=0.05)
+        cfg = po.PRMConfig(K=2, beta=0.9, gamma=0.3, wd=0.1, lr=0.05, gamma_on_refresh=gamma_on_refresh)
         s = math.sqrt(max(1.0, m / n))
         nf = np.linalg.norm(G)
-        y = nf / (nf + 1e-7)
-        for _ in range(5):
-            y = a * y + b * y ** 3 + c * y ** 5
+        y = _quintic5(nf / (nf + 1e-7))
+        g_ref = 0.3 if gamma_on_refresh else 1.0
         Wn, Mn, D, rho = po.step_matrix(W, np.zeros((m, n)), G, 0, cfg)
         assert rho == 1
         np.testing.assert_allclose(Mn, G)
-        expect_D = s * y * np.outer(u / np.linalg.norm(u), v / np.linalg.norm(v))
+        expect_D = g_ref * s * y * np.outer(u / np.linalg.norm(u), v / np.linalg.norm(v))
         np.testing.assert_allclose(D, expect_D, rtol=1e-12, atol=1e-14)
         np.testing.assert_allclose(Wn, (1 - 0.05 * 0.1) * W - 0.05 * expect_D, rtol=1e-12)
         Wn, Mn, D, rho = po.step_matrix(W, np.zeros((m, n)), G, 1, cfg)
@@ -332,6 +428,37 @@ def test_step_rank_one_closed_forms():
             expect = 0.3 * s * np.outer(u / np.linalg.norm(u), np.sign(v))
         np.testing.assert_allclose(D, expect, rtol=1e-12, atol=1e-14)
         np.testing.assert_allclose(Wn, (1 - 0.05 * 0.1) * W - 0.05 * expect, rtol=1e-12)
+
+
+def test_step_rank_one_closed_forms():
+    pin_step_rank_one_closed_forms()
+
+
+def test_scalar_controlled_ablation_closed_forms():
+    pin_step_rank_one_closed_forms(gamma_on_refresh=True)
+
+
+def pin_scalar_controlled_scales_refresh_only():
+    """Scalar-controlled ablation on a full-rank input: over a trajectory, the
+    refresh directions are exactly gamma times those of the paper's method and
+    the row-wise directions are identical (the state never depends on D)."""
+    rng = np.random.default_rng(23)
+    for (m, n) in [(12, 30), (30, 12)]:
+        a = po.PRMConfig(K=3, gamma=0.15)
+        b = po.PRMConfig(K=3, gamma=0.15, gamma_on_refresh=True)
+        Wa = Wb = rng.standard_normal((m, n))
+        Ma = Mb = rng.standard_normal((m, n))
+        for t in range(6):
+            G = rng.standard_normal((m, n))
+            Wa, Ma, Da, ra = po.step_matrix(Wa, Ma, G, t, a)
+            Wb, Mb, Db, rb = po.step_matrix(Wb, Mb, G, t, b)
+            assert ra == rb == (1 if t % 3 == 0 else 0)
+            np.testing.assert_array_equal(Mb, Ma)
+            np.testing.assert_allclose(Db, (0.15 if ra else 1.0) * Da, rtol=1e-13, atol=1e-16)
+
+
+def test_scalar_controlled_scales_refresh_only():
+    pin_scalar_controlled_scales_refresh_only()
 
 
 def test_gamma_only_on_rownorm_branch_and_wd_uses_eta():
@@ -389,17 +516,114 @@ def test_mutations_are_caught(monkeypatch):
     monkeypatch.undo()
     assert svd_pin_holds()
 
-    # RowNorm clamp before the sqrt (max(||x||^2, eps)) fails the eps pin
-    def bad_rownorm(X, eps):
-        nu = np.sqrt(np.maximum(np.sum(X * X, axis=1), eps))
-        return X / nu[:, None]
-    Xs = np.zeros((1, 4)); Xs[0, :2] = [3e-3, 4e-3]
-    assert not np.allclose(bad_rownorm(Xs, 1e-2), Xs / 1e-2)
 
-    # wrong orientation (normalizing stored rows of a tall matrix) fails the
-    # sharded/column pin
-    M = rng.standard_normal((30, 6))
-    good = po.orient_inv(po.rownorm(po.orient(M), 1e-8), 30, 6)
-    wrong = po.rownorm(M, 1e-8)
-    assert np.allclose(np.linalg.norm(good, axis=0), 1.0)
-    assert not np.allclose(np.linalg.norm(wrong, axis=0), 1.0)
+def _raises(pin, *args):
+    try:
+        pin(*args)
+    except AssertionError:
+        return True
+    return False
+
+
+def test_rownorm_mutations_fail_their_pins(monkeypatch):
+    """RowNorm mistakes planted into the oracle itself."""
+    pin_rownorm_eps_clamp_after_sqrt()
+    pin_sharded_tall_rownorm()
+    real = po.rownorm
+
+    # the clamp taken before the square root: max(||x||^2, eps)
+    def clamp_before_sqrt(X, eps):
+        X = np.asarray(X, dtype=np.float64)
+        return X / np.sqrt(np.maximum(np.sum(X * X, axis=1), eps))[:, None]
+    monkeypatch.setattr(po, "rownorm", clamp_before_sqrt)
+    assert _raises(pin_rownorm_eps_clamp_after_sqrt)
+    # the clamp dropped
+    monkeypatch.setattr(po, "rownorm", lambda X, eps: X / np.linalg.norm(X, axis=1, keepdims=True))
+    assert _raises(pin_rownorm_eps_clamp_after_sqrt)
+    # the squared norm in the denominator
+    monkeypatch.setattr(po, "rownorm", lambda X, eps: X / np.maximum(np.sum(X * X, axis=1), eps)[:, None])
+    assert _raises(pin_rownorm_eps_clamp_after_sqrt)
+    monkeypatch.setattr(po, "rownorm", real)
+    # a tall matrix normalized along its stored rows (no orientation)
+    monkeypatch.setattr(po, "orient", lambda M: M)
+    monkeypatch.setattr(po, "orient_inv", lambda X, m, n: X)
+    assert _raises(pin_sharded_tall_rownorm)
+    assert _raises(pin_step_rank_one_closed_forms)
+    monkeypatch.undo()
+    pin_sharded_tall_rownorm()
+    pin_step_rank_one_closed_forms()
+
+
+def _step_with(U_of):
+    """step_matrix with the direction input replaced by U_of(M_old, M_new, G, cfg)."""
+    def step_matrix(W, M, G, t, cfg, lr=None):
+        eta = cfg.lr if lr is None else lr
+        W, M, G = (np.asarray(x, dtype=np.float64) for x in (W, M, G))
+        M_new = po.momentum_update(M, G, cfg.beta, cfg.ema_dampening)
+        D, rho = po.direction(U_of(M, M_new, G, cfg), t, cfg)
+        return (1.0 - eta * cfg.wd) * W - eta * D, M_new, D, rho
+    return step_matrix
+
+
+def test_nesterov_mutations_fail_their_pins(monkeypatch):
+    """Nesterov mistakes planted into the oracle's step."""
+    pin_nesterov_lookahead()
+    pin_nesterov_constructed_target()
+    # the look-ahead built from the momentum before this step's update
+    monkeypatch.setattr(po, "step_matrix",
+                        _step_with(lambda Mo, Mn, G, c: G + c.beta * Mo if c.nesterov else Mn))
+    assert _raises(pin_nesterov_lookahead)
+    assert _raises(pin_nesterov_constructed_target)
+    # beta dropped from the look-ahead
+    monkeypatch.setattr(po, "step_matrix", _step_with(lambda Mo, Mn, G, c: G + Mn if c.nesterov else Mn))
+    assert _raises(pin_nesterov_lookahead)
+    assert _raises(pin_nesterov_constructed_target)
+    # the flag ignored
+    monkeypatch.setattr(po, "step_matrix", _step_with(lambda Mo, Mn, G, c: Mn))
+    assert _raises(pin_nesterov_lookahead)
+    assert _raises(pin_nesterov_constructed_target)
+    # the correct form passes through the same wrapper
+    monkeypatch.setattr(po, "step_matrix",
+                        _step_with(lambda Mo, Mn, G, c: G + c.beta * Mn if c.nesterov else Mn))
+    pin_nesterov_lookahead()
+    pin_nesterov_constructed_target()
+
+
+def test_scalar_controlled_mutations_fail_their_pins(monkeypatch):
+    """gamma mistakes planted into the oracle's direction map."""
+    pin_step_rank_one_closed_forms(True)
+    pin_scalar_controlled_scales_refresh_only()
+    real = po.direction
+
+    def with_refresh_gamma(g_of):
+        def direction(U, t, cfg):
+            D, rho = real(U, t, po.PRMConfig(**{**cfg.__dict__, "gamma_on_refresh": False}))
+            return (g_of(cfg) * D if rho else D), rho
+        return direction
+    # the ablation flag ignored (no gamma on the refresh branch)
+    monkeypatch.setattr(po, "direction", with_refresh_gamma(lambda c: 1.0))
+    assert _raises(pin_step_rank_one_closed_forms, True)
+    assert _raises(pin_scalar_controlled_scales_refresh_only)
+    # gamma applied twice
+    monkeypatch.setattr(po, "direction", with_refresh_gamma(lambda c: c.gamma ** 2 if c.gamma_on_refresh else 1.0))
+    assert _raises(pin_step_rank_one_closed_forms, True)
+    assert _raises(pin_scalar_controlled_scales_refresh_only)
+    # gamma on the refresh branch of the paper's method too
+    monkeypatch.setattr(po, "direction", with_refresh_gamma(lambda c: c.gamma))
+    assert _raises(pin_step_rank_one_closed_forms)
+    # the correct rule passes through the same wrapper
+    monkeypatch.setattr(po, "direction", with_refresh_gamma(lambda c: c.gamma if c.gamma_on_refresh else 1.0))
+    pin_step_rank_one_closed_forms(True)
+    pin_step_rank_one_closed_forms()
+    pin_scalar_controlled_scales_refresh_only()
+
+
+def test_config_rejects_nonpositive_clamps():
+    # a zero eps_ns would turn a zero momentum into 0/0 in the input scaling
+    for kw in ({"eps_ns": 0.0}, {"eps_rownorm": 0.0}, {"K": 0}):
+        with pytest.raises(ValueError):
+            po.PRMConfig(**kw)
+    cfg = po.PRMConfig(K=1, beta=0.0)
+    _, _, D, rho = po.step_matrix(np.ones((3, 5)), np.zeros((3, 5)), np.zeros((3, 5)), 0, cfg)
+    assert rho == 1
+    np.testing.assert_array_equal(D, 0.0)
