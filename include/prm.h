@@ -255,6 +255,32 @@ int prm_peak_mfma(void* hip_stream, int32_t iters, double* tflops, double* clock
 int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* write_gbs, double* copy_gbs,
                  double* rowwise_gbs);
 
+/* ---- Allocation-free step ------------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  One
+ * optimizer step t of ONE matrix (rows x cols, W param, G grad, M momentum:
+ * device pointers, 16-byte aligned, as in prm_step) without a context: the
+ * same kernels as prm_step on a context created for that matrix alone, with
+ * bitwise the same W and M.  Nothing is allocated (no hipMalloc, hipFree or
+ * allocating library call) and nothing waits for the GPU: after validation the
+ * call enqueues a small set-up kernel and the step's kernels on `hip_stream`,
+ * on the CURRENT device.  *did_refresh (nullable) receives rho_t.
+ *
+ * Scratch: the descriptor, work lists and workspace (the NS5 iterates and Gram
+ * factors on refresh steps, a tall matrix's column statistics on row-wise
+ * steps) live in one static device array of PRM_NOALLOC_SCRATCH_BYTES per GPU,
+ * which the library holds on every GPU it runs on until the process ends.  A
+ * step that needs more is refused with PRM_ENOMEM before anything is enqueued
+ * (refresh steps fit matrices up to about 3072 x 18432; row-wise steps of wide
+ * matrices need no workspace).  Every call on one GPU uses the same array:
+ * calls that overlap in time on one GPU (on other streams or threads) RACE
+ * and give wrong results; calls ordered on one stream are safe, and every byte
+ * a kernel reads from the array is written earlier in the same call.
+ * cfg->workspace_budget_bytes is ignored.  Errors as in prm_init / prm_step. */
+#define PRM_NOALLOC_SCRATCH_BYTES (256ull << 20)
+int prm_step_noalloc(const prm_config* cfg, int64_t rows, int64_t cols, void* param, const void* grad,
+                     float* momentum, int64_t step, float lr, int32_t* did_refresh, void* hip_stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* prm_last_error(void);
 

@@ -14,7 +14,7 @@ import os
 __all__ = [
     "PRMError", "Config", "KernelStats", "Optimizer", "AdamWConfig", "AuxAdamW", "load",
     "config_default", "adamw_config_default",
-    "schedule_is_refresh", "plan_workspace_bytes", "PRM_OK", "PRM_EINVAL", "PRM_EDTYPE", "PRM_EALIGN",
+    "schedule_is_refresh", "plan_workspace_bytes", "step_noalloc", "NOALLOC_SCRATCH_BYTES", "PRM_OK", "PRM_EINVAL", "PRM_EDTYPE", "PRM_EALIGN",
     "PRM_ENOMEM", "PRM_EHIP", "F32", "BF16", "KERNEL_CLASSES",
 ]
 
@@ -24,6 +24,7 @@ PRM_OK, PRM_EINVAL, PRM_EDTYPE, PRM_EALIGN, PRM_ENOMEM, PRM_EHIP = 0, -1, -2, -3
 F32, BF16 = 0, 1
 SCALE_ONE, SCALE_SQRT_ASPECT, SCALE_RMS_0P2 = 0, 1, 2
 NUM_KERNEL_CLASSES = 10
+NOALLOC_SCRATCH_BYTES = 256 << 20  # PRM_NOALLOC_SCRATCH_BYTES
 KERNEL_CLASSES = ("rw_wide", "rw_generic", "rw_tall_stats", "rw_tall_finalize", "rw_tall_apply",
                   "ns_prologue", "ns_alpha", "ns_gram", "ns_poly", "ns_apply")
 
@@ -93,6 +94,9 @@ def load() -> ctypes.CDLL:
     L.prm_plan_workspace_bytes.argtypes = [ctypes.c_int32, i64p, i64p, ctypes.POINTER(Config),
                                            ctypes.POINTER(ctypes.c_uint64)]
     L.prm_plan_workspace_bytes.restype = ctypes.c_int
+    L.prm_step_noalloc.argtypes = [ctypes.POINTER(Config), ctypes.c_int64, ctypes.c_int64, P, P, P,
+                                   ctypes.c_int64, ctypes.c_float, ctypes.POINTER(ctypes.c_int32), P]
+    L.prm_step_noalloc.restype = ctypes.c_int
     L.prm_profile_enable.argtypes = [P, ctypes.c_int32]
     L.prm_profile_enable.restype = ctypes.c_int
     L.prm_profile_read.argtypes = [P, ctypes.POINTER(KernelStats), ctypes.c_int32]
@@ -181,6 +185,27 @@ def peak_hbm(nbytes: int = 4 << 30, stream=None) -> dict:
 
 def _ptr(x) -> int:
     return x if isinstance(x, int) else x.data_ptr()
+
+
+def step_noalloc(cfg: Config, param, grad, momentum, step: int, lr: float = -1.0, stream=None) -> int:
+    """One step of one matrix through prm_step_noalloc (no context, no device
+    allocation; see prm.h); returns rho_t.  Tensors (or raw device pointers):
+    contiguous W in ``cfg.param_dtype``, G in ``cfg.grad_dtype``, fp32 M, all of
+    one shape (rows, cols)."""
+    if not isinstance(param, int):
+        shape = tuple(param.shape)
+        for x, dt, what in ((param, _DT[cfg.param_dtype], "param"), (grad, _DT[cfg.grad_dtype], "grad"),
+                            (momentum, "float32", "momentum")):
+            if not x.is_cuda or tuple(x.shape) != shape or len(shape) != 2 or not x.is_contiguous() \
+                    or str(x.dtype) != f"torch.{dt}":
+                raise ValueError(f"{what}: need a contiguous 2-D {dt} device tensor of shape {shape}")
+        rows, cols = shape
+    else:
+        raise ValueError("step_noalloc needs tensors (the shape comes from them)")
+    rho = ctypes.c_int32(-1)
+    _check(load().prm_step_noalloc(ctypes.byref(cfg), rows, cols, _ptr(param), _ptr(grad), _ptr(momentum),
+                                   int(step), float(lr), ctypes.byref(rho), _stream_handle(stream)))
+    return rho.value
 
 
 _DT = {F32: "float32", BF16: "bfloat16"}

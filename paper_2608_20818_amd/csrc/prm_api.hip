@@ -13,6 +13,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -382,6 +383,40 @@ void build_lists(Plan& P, const prm_config* cfg) {
   if (P.items.empty()) P.items.push_back(Item{0, 0, 0, 0});
 }
 
+// Static descriptor fields of every matrix: shape, scale, and its regions of
+// the NS5 chunk area, the small per-matrix scalars and the tall statistics
+// (caller pointers are filled in before a step).
+void fill_descs(const Plan& P, char* chunk_base, char* small_base, char* tall_base, std::vector<MatDesc>& desc) {
+  desc.assign(P.n, MatDesc{});
+  for (int i = 0; i < P.n; ++i) {
+    MatDesc& d = desc[i];
+    d.m = P.m[i];
+    d.n = P.nn[i];
+    d.s = P.s[i];
+    d.tall = P.tall[i];
+    d.rp = P.rp[i];
+    d.cp = P.cp[i];
+    const uint64_t xs = align256((uint64_t)d.rp * d.cp * 2), gs = align256((uint64_t)d.rp * d.rp * 2),
+                   vs = align256((uint64_t)d.rp * 4);
+    char* w = chunk_base + P.ws_off[i];
+    d.XT = (uint16_t*)w;
+    d.XTn = (uint16_t*)(w + xs);
+    d.Ao = (uint16_t*)(w + 2 * xs);
+    d.Bo = (uint16_t*)(w + 2 * xs + gs);
+    d.dA = (float*)(w + 2 * xs + 2 * gs);
+    d.dB = (float*)(w + 2 * xs + 2 * gs + vs);
+    d.ptiles_m = (int32_t)((d.tall ? d.cp : d.rp) / kPrologueTile);
+    d.ptiles_n = (int32_t)((d.tall ? d.rp : d.cp) / kPrologueTile);
+    d.partial = (float*)(small_base + P.small_off[i]);
+    d.alpha = d.partial + (int64_t)d.ptiles_m * d.ptiles_n;
+    if (d.tall) {
+      d.nrb = P.nrb[i];
+      d.colpart = (float*)(tall_base + P.tall_off[i]);
+      d.colinv = d.colpart + (int64_t)d.nrb * d.n;
+    }
+  }
+}
+
 struct ProfRec {
   int cls;
   hipEvent_t e0, e1;
@@ -660,6 +695,86 @@ int check_adamw_config(const prm_adamw_config* c) {
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// allocation-free single-matrix step (prm_step_noalloc)
+//
+// Its descriptor, work lists and workspace live in `scratch`, a file-scope
+// device array.  In host code the name `scratch` is only a stand-in for the
+// symbol: its device address, which differs per GPU, comes from
+// hipGetSymbolAddress (taken once per device, with that device current) and
+// is the only handle host code passes on.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) char scratch[PRM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev` (the current device).
+int noalloc_scratch(int dev, char** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(PRM_EINVAL, "device %d is outside the supported range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(PRM_EHIP, "hipGetSymbolAddress of the scratch array failed on device %d: %s", dev,
+                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return PRM_OK;
+}
+
+// One work list of the single matrix: `count` items from position `off`,
+// enumerated row-major over a grid with `dim` columns, or (upper) over the
+// tiles (a, b), b >= a, of a dim x dim grid, row by row.  The order differs
+// from the context's lists (those are arranged for L2 sharing across
+// matrices); each item's output tile is computed the same way either way.
+struct NoallocSeg {
+  int32_t off, count, dim, upper;
+};
+constexpr int kNoallocSegs = 4;
+struct NoallocSetup {
+  MatDesc d;
+  NoallocSeg seg[kNoallocSegs];
+  int32_t nseg;
+  int32_t nints;  // int lists: all zero for one matrix (matrix 0, first block 0)
+};
+
+// Writes the descriptor, the int lists and the work lists of one call into
+// the scratch array; thread i writes entry i of every list.  Everything comes
+// in the kernel arguments, so no host buffer has to outlive the call.
+__global__ __launch_bounds__(256) void noalloc_setup_kernel(NoallocSetup s, MatDesc* desc, int32_t* ints,
+                                                            Item* items) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i == 0) *desc = s.d;
+  if (i < s.nints) ints[i] = 0;
+  for (int j = 0; j < s.nseg; ++j) {
+    const NoallocSeg g = s.seg[j];
+    if (i >= g.count) continue;
+    int32_t a, b;
+    if (g.upper) {
+      // i < dim (dim + 1) / 2: row a holds dim - a tiles
+      int32_t k = (int32_t)i;
+      a = 0;
+      while (k >= g.dim - a) {
+        k -= g.dim - a;
+        ++a;
+      }
+      b = a + k;
+    } else {
+      a = (int32_t)(i / g.dim);
+      b = (int32_t)(i % g.dim);
+    }
+    items[g.off + i] = Item{0, a, b, 0};
+  }
+}
+
+}  // namespace
+
 extern "C" {
 
 void prm_config_default(prm_config* cfg) {
@@ -748,38 +863,9 @@ int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* 
     e = hipMemcpy(c->d_items, P.items.data(), sizeof(Item) * P.items.size(), hipMemcpyHostToDevice);
   if (e != hipSuccess) return cleanup(fail(PRM_EHIP, "hipMemcpy failed: %s", hipGetErrorString(e)));
   // static descriptor fields
-  c->desc.assign(P.n, MatDesc{});
   c->last_ptrs.assign(4 * (size_t)P.n, nullptr);
-  char* chunk_base = c->d_ws;
   char* small_base = c->d_ws + align256(P.chunk_bytes);
-  char* tall_base = small_base + P.small_bytes;
-  for (int i = 0; i < P.n; ++i) {
-    MatDesc& d = c->desc[i];
-    d.m = P.m[i];
-    d.n = P.nn[i];
-    d.s = P.s[i];
-    d.tall = P.tall[i];
-    d.rp = P.rp[i];
-    d.cp = P.cp[i];
-    const uint64_t xs = align256((uint64_t)d.rp * d.cp * 2), gs = align256((uint64_t)d.rp * d.rp * 2),
-                   vs = align256((uint64_t)d.rp * 4);
-    char* w = chunk_base + P.ws_off[i];
-    d.XT = (uint16_t*)w;
-    d.XTn = (uint16_t*)(w + xs);
-    d.Ao = (uint16_t*)(w + 2 * xs);
-    d.Bo = (uint16_t*)(w + 2 * xs + gs);
-    d.dA = (float*)(w + 2 * xs + 2 * gs);
-    d.dB = (float*)(w + 2 * xs + 2 * gs + vs);
-    d.ptiles_m = (int32_t)((d.tall ? d.cp : d.rp) / kPrologueTile);
-    d.ptiles_n = (int32_t)((d.tall ? d.rp : d.cp) / kPrologueTile);
-    d.partial = (float*)(small_base + P.small_off[i]);
-    d.alpha = d.partial + (int64_t)d.ptiles_m * d.ptiles_n;
-    if (d.tall) {
-      d.nrb = P.nrb[i];
-      d.colpart = (float*)(tall_base + P.tall_off[i]);
-      d.colinv = d.colpart + (int64_t)d.nrb * d.n;
-    }
-  }
+  fill_descs(P, c->d_ws, small_base, small_base + P.small_bytes, c->desc);
   e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return cleanup(fail(PRM_EHIP, "hipStreamSynchronize failed: %s", hipGetErrorString(e)));
   *out = c;
@@ -1069,6 +1155,101 @@ int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* wri
   (void)hipFree(y);
   (void)hipFree(sink);
   return rc;
+}
+
+int prm_step_noalloc(const prm_config* cfg, int64_t rows, int64_t cols, void* param, const void* grad,
+                     float* momentum, int64_t step, float lr, int32_t* did_refresh, void* hip_stream) {
+  if (!cfg) return fail(PRM_EINVAL, "cfg is NULL");
+  if (step < 0) return fail(PRM_EINVAL, "step must be >= 0 (got %lld)", (long long)step);
+  const float eta = lr < 0.f ? cfg->lr : lr;
+  if (!std::isfinite(eta)) return fail(PRM_EINVAL, "lr must be finite");
+  // the workspace cap is the scratch array, checked below
+  prm_config c2 = *cfg;
+  c2.workspace_budget_bytes = 1ull << 62;
+  Plan P;
+  int rc = make_plan(1, &rows, &cols, &c2, P);
+  if (rc) return rc;
+  const void* ps[3] = {param, grad, momentum};
+  for (int k = 0; k < 3; ++k) {
+    if (!ps[k]) return fail(PRM_EINVAL, "NULL device pointer (argument %d)", k);
+    if ((uintptr_t)ps[k] % 16) return fail(PRM_EALIGN, "pointer %d is not 16-byte aligned", k);
+  }
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  for (int k = 0; k < 3; ++k) {
+    rc = check_device_ptr(dev, ps[k], "matrix", 0, k);
+    if (rc) return rc;
+  }
+  const int rho = refresh_of(c2, step);
+  // scratch layout: descriptor | int lists | work lists | per-matrix scalars |
+  // NS5 workspace (refresh) or tall column statistics (row-wise)
+  const int64_t T = P.rp[0] / kNsTile, tc = P.cp[0] / kNsTile;
+  const int64_t pn = (P.tall[0] ? P.rp[0] : P.cp[0]) / kPrologueTile;
+  const int64_t pm = (P.tall[0] ? P.cp[0] : P.rp[0]) / kPrologueTile;
+  const int64_t slabs = (P.nn[0] + 255) / 256;
+  const int64_t nitems = rho ? pm * pn + T * (T + 1) + tc * T : (P.tall[0] ? (int64_t)P.nrb[0] * slabs + slabs : 0);
+  const uint64_t off_ints = align256(sizeof(MatDesc)), off_items = off_ints + 256;
+  const uint64_t off_small = off_items + align256((uint64_t)std::max<int64_t>(nitems, 1) * sizeof(Item));
+  const uint64_t off_big = off_small + align256(P.small_bytes);
+  const uint64_t need = off_big + (rho ? P.chunk_bytes : P.tall_bytes);
+  if (need > PRM_NOALLOC_SCRATCH_BYTES)
+    return fail(PRM_ENOMEM, "a %s step of a %lld x %lld matrix needs %llu scratch bytes; the allocation-free step has %llu",
+                rho ? "refresh" : "row-wise", (long long)rows, (long long)cols, (unsigned long long)need,
+                (unsigned long long)PRM_NOALLOC_SCRATCH_BYTES);
+  build_lists(P, &c2);
+  if (P.ints.size() > 64) return fail(PRM_EHIP, "internal: %zu int list entries", P.ints.size());
+  for (int32_t v : P.ints)
+    if (v != 0) return fail(PRM_EHIP, "internal: nonzero int list entry for one matrix");
+  // the work lists this step launches, packed from item 0
+  NoallocSetup s;
+  std::memset(&s, 0, sizeof(s));
+  int32_t pos = 0;
+  auto add = [&](size_t& off, size_t count, int64_t want, int64_t dim, int upper) {
+    if ((int64_t)count != want || s.nseg == kNoallocSegs) return false;
+    off = (size_t)pos;
+    s.seg[s.nseg++] = NoallocSeg{pos, (int32_t)count, (int32_t)dim, upper};
+    pos += (int32_t)count;
+    return true;
+  };
+  bool ok = true;
+  if (rho) {
+    Chunk& ch = P.chunks[0];
+    ok = add(ch.off_prologue, ch.prologue.size(), pm * pn, pn, 0) &&
+         add(ch.off_gram, ch.gram.size(), T * (T + 1) / 2, T, 1) &&
+         add(ch.off_poly, ch.poly.size(), T * (T + 1) / 2, T, 1) &&
+         add(ch.off_apply, ch.apply.size(), tc * T, T, 0);
+  } else if (P.tall[0]) {
+    const bool v4 = !P.tall_items4.empty();
+    ok = add(v4 ? P.off_tall4 : P.off_tall1, v4 ? P.tall_items4.size() : P.tall_items1.size(),
+             (int64_t)P.nrb[0] * slabs, slabs, 0) &&
+         add(P.off_fin, P.fin_items.size(), slabs, slabs, 0);
+  }
+  if (!ok || pos != nitems) return fail(PRM_EHIP, "internal: work list sizes disagree with the plan");
+  s.nints = (int32_t)P.ints.size();
+  char* base = nullptr;
+  rc = noalloc_scratch(dev, &base);
+  if (rc) return rc;
+  std::vector<MatDesc> desc;
+  fill_descs(P, base + off_big, base + off_small, base + off_big, desc);
+  s.d = desc[0];
+  s.d.W = param;
+  s.d.G = grad;
+  s.d.M = momentum;
+  s.d.D = nullptr;
+  if (did_refresh) *did_refresh = rho;
+  prm_ctx c;
+  c.cfg = c2;
+  c.stream = (hipStream_t)hip_stream;
+  c.device = dev;
+  c.d_desc = reinterpret_cast<MatDesc*>(base);
+  c.d_ints = reinterpret_cast<int32_t*>(base + off_ints);
+  c.d_items = reinterpret_cast<Item*>(base + off_items);
+  const int64_t threads = std::max<int64_t>({(int64_t)pos, (int64_t)s.nints, 1});
+  noalloc_setup_kernel<<<dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, c.stream>>>(s, c.d_desc, c.d_ints,
+                                                                                           c.d_items);
+  HIP_TRY(hipGetLastError());
+  c.plan = std::move(P);
+  return rho ? refresh_step(&c, eta, false) : rowwise_step(&c, eta, false);
 }
 
 const char* prm_last_error(void) { return g_err.c_str(); }
