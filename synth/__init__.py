@@ -182,21 +182,23 @@ def host_factors(workload: int, mat: int, m: int, n: int, k: int):
 
 
 def host_matrix(workload: int, mat: int, m: int, n: int, k: int, *, param_dtype: str,
-                grad_dtype: str, beta: float = 0.95, steps=(0,)):
+                grad_dtype: str, beta: float = 0.95, steps=(0,), noise: float = 0.01):
     """(W0, M0, {t: G_t}) for one matrix as float64 arrays holding exact storage values.
 
-    W0 in ``param_dtype``; M0 in fp32; gradients in ``grad_dtype``.
+    W0 in ``param_dtype``; M0 in fp32; gradients in ``grad_dtype``.  ``noise``
+    is the standard deviation of the Gaussian term of each gradient (0.01 in
+    every workload; smaller values give signal-dominated momenta).
     """
     U, V = host_factors(workload, mat, m, n, k)
     s = spectrum(k)
     W0 = 0.02 * host_rng(workload, mat, "W").standard_normal((m, n))
     sig_m = 1.0 + beta + beta * beta
-    noise_m = 0.01 * math.sqrt(1.0 + beta ** 2 + beta ** 4)
+    noise_m = noise * math.sqrt(1.0 + beta ** 2 + beta ** 4)
     M0 = (U * (sig_m * s)) @ V.T + noise_m * host_rng(workload, mat, "M").standard_normal((m, n))
     grads = {}
     for t in steps:
         grads[t] = to_dtype_values(
-            (U * s) @ V.T + 0.01 * host_rng(workload, mat, "G", t).standard_normal((m, n)),
+            (U * s) @ V.T + noise * host_rng(workload, mat, "G", t).standard_normal((m, n)),
             grad_dtype)
     return to_dtype_values(W0, param_dtype), to_dtype_values(M0, "f32"), grads
 

@@ -82,3 +82,35 @@ def bf16_write_bound(W_gpu, W_or, D_gpu, D_or, lr) -> float:
     ulp = synth.bf16_ulp(W_gpu)
     bound = 0.5 * ulp + eta * np.abs(D_gpu - D_or) * 1.001 + 2.0 ** -22 * (np.abs(W_or) + eta * np.abs(D_or)) + 1e-38
     return float(np.max(np.abs(W_gpu - W_or) / bound))
+
+
+def ns_chunks(shapes, budget=32 << 30, tile=256):
+    """Which NS5 workspace chunk each matrix lands in, as the library's planner
+    packs them (include/prm.h, prm_init): matrices sorted by padded oriented
+    shape (r desc, then c desc, ties in list order) are packed in order into
+    chunks of at most `budget` bytes, each matrix taking 4 rp cp + 4 rp^2 +
+    8 rp bytes (regions aligned to 256 bytes).  Returns (chunk index per
+    matrix, largest chunk's bytes); tests check the latter against
+    prm_plan_workspace_bytes."""
+    def a256(x):
+        return (x + 255) // 256 * 256
+    rp = [-(-min(m, n) // tile) * tile for m, n in shapes]
+    cp = [-(-max(m, n) // tile) * tile for m, n in shapes]
+    order = sorted(range(len(shapes)), key=lambda i: (-rp[i], -cp[i], i))
+    chunk = [0] * len(shapes)
+    k, cur, biggest = -1, 0, 0
+    for i in order:
+        need = 2 * a256(rp[i] * cp[i] * 2) + 2 * a256(rp[i] * rp[i] * 2) + 2 * a256(rp[i] * 4)
+        if k < 0 or cur + need > budget:
+            k, cur = k + 1, 0
+        chunk[i] = k
+        cur += need
+        biggest = max(biggest, cur)
+    return chunk, biggest
+
+
+def row_errors(A, B):
+    """Relative error of every row of A against the same row of B."""
+    num = np.linalg.norm(A - B, axis=1)
+    den = np.maximum(np.linalg.norm(B, axis=1), 1e-300)
+    return num / den

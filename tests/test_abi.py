@@ -316,3 +316,22 @@ def test_gemm_inline_dma_leaves_m0_to_the_compiler(tmp_path):
     readers, asm_dma, bad = _m0_check(out.read_text())
     assert asm_dma > 0 and readers > 0
     assert not bad, bad[:5]
+
+
+def test_fullsize_sample_covers_every_chunk():
+    # the test's replica of the chunk packing agrees with the library's planner
+    # (largest chunk + per-matrix scalars + tall statistics = its total), and the
+    # DiT-15B refresh sample reaches every chunk and every matrix kind
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import prm_case as pc
+    import test_gpu_fullsize as fs
+    cfg = prm.config_default()
+    for wi in (1, 2, 3, 4):
+        shapes = synth.WORKLOADS[wi].shapes
+        chunk, biggest = pc.ns_chunks(shapes)
+        assert prm.plan_workspace_bytes(shapes, cfg) == (biggest + 255) // 256 * 256 + sum(
+            prm.plan_workspace_bytes([s], cfg) - pc.ns_chunks([s])[1] for s in shapes), wi
+        sample = fs.REFRESH_SAMPLE[wi]
+        assert {chunk[i] for i in sample} == set(chunk), wi
+        assert {i % 5 for i in sample} == set(range(5)), wi
+    assert len(set(pc.ns_chunks(synth.WORKLOADS[4].shapes)[0])) == 4
