@@ -51,7 +51,7 @@ def parse():
                     help="workload index: 0 tiny, 1 DiT-1.3B, 2 DiT-4B (default), 3 DiT-9B, 4 DiT-15B")
     ap.add_argument("--K", type=int, default=None, help="refresh period (default: the workload's)")
     ap.add_argument("--variant", action="append", default=[],
-                    choices=["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh"],
+                    choices=["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh", "ns_plain"],
                     help="ablation flags of the configuration (repeatable); the default is the paper's method")
     ap.add_argument("--grad-dtype", choices=["bf16", "f32"], default=None,
                     help="gradient storage dtype (default: the workload's, bf16 for the DiT-shaped sets)")
@@ -117,27 +117,6 @@ def counter_mfma(workload: str):
     if t.get("kernel_source_sha256_16") != kernel_source_hash() or t.get("workload") != workload:
         return None
     return t["classes"]
-
-
-def executed_ns5_flops(shapes):
-    """FLOPs the NS5 GEMM kernels execute in one refresh step (MFMA work
-    actually issued), as opposed to the algorithmic 20 r^2 c + 10 r^3: every
-    matrix is padded to 256 x 256 tiles; the Gram and the square compute only
-    the tiles on and above the diagonal (T (T + 1) / 2 of T^2); the apply runs
-    every tile plus, per wave, 64 MFMAs for the diagonal term a X + dB X
-    against 64 nk regular ones (nk = rp / 64 stages of K)."""
-    tile = 256
-    total = {"ns_gram": 0.0, "ns_poly": 0.0, "ns_apply": 0.0}
-    for m, n in shapes:
-        r, c = min(m, n), max(m, n)
-        rp, cp = -(-r // tile) * tile, -(-c // tile) * tile
-        T = rp // tile
-        upper = T * (T + 1) // 2
-        nk = rp // 64
-        total["ns_gram"] += 5 * upper * 2.0 * tile * tile * cp
-        total["ns_poly"] += 5 * upper * 2.0 * tile * tile * rp
-        total["ns_apply"] += 5 * (cp // tile) * T * 2.0 * tile * tile * rp * (1 + 1 / nk)
-    return total
 
 
 def make_inputs(wl_idx, wl, device):
@@ -369,14 +348,12 @@ def main():
     elems = sum(m * n for m, n in shapes)
     rw_bytes = elems * (gb + 4 + 4 + 2 * wb)
     ns_flops = sum(po.ns5_flops(m, n) for m, n in shapes)
-    exec_flops = executed_ns5_flops(shapes)
-    ns_exec = sum(exec_flops.values())
-    # two readings of "MFMA %" of the refresh step: the paper's algorithmic
-    # FLOPs over the whole step time (what a dense GEMM chain would need), and
-    # the FLOPs the kernels actually issue (the symmetric products compute
-    # only upper tiles, so this is the utilisation of the matrix cores)
+    # the paper's NS5 FLOPs (20 r^2 c + 10 r^3 per matrix) over the refresh
+    # time: the effective rate of the refresh against the bf16 peak.  The
+    # kernels issue fewer (upper tiles of symmetric products, the factored
+    # form of wide matrices); their own rate is refresh_executed_mfma_frac.
     refresh_alg_frac = ns_flops / (T_ref * 1e-3) / (PEAK_BF16_TFLOPS * 1e12) if ref else None
-    refresh_exec_frac = ns_exec / (T_ref * 1e-3) / (PEAK_BF16_TFLOPS * 1e12) if ref else None
+    ns_exec, refresh_exec_frac = None, None
     rowwise_hbm_frac = rw_bytes / (T_rw * 1e-3) / (PEAK_HBM_GBS * 1e9) if rw else None
 
     kernels, roofline, roofline_rw = None, None, None
@@ -410,15 +387,19 @@ def main():
                     "alg_per_launch": k["alg_bytes"] / k["launches"]}
 
         roofline = roof(dom, kd)
-        # executed MFMA rate of each GEMM kind over its own launches (per refresh
-        # step: the profiled period holds one refresh)
+        # executed MFMA FLOPs (what the matrix cores run, from libprm's own
+        # tile counts) of each GEMM kind over its launches in the profiled
+        # period, which holds one refresh step
         gemm_exec_frac = {}
-        for kname, fl in exec_flops.items():
+        ns_kinds = ("ns_gram", "ns_poly", "ns_sprod", "ns_apply")
+        for kname in ns_kinds:
             k = kernels[kname]
             if k["launches"] and k["total_ms"] > 0:
-                gemm_exec_frac[kname] = fl / (k["total_ms"] * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
-        if roofline is not None and roofline["kernel"] in exec_flops:
-            roofline["executed_per_launch"] = exec_flops[roofline["kernel"]] / roofline["launches"]
+                gemm_exec_frac[kname] = k["exec_flops"] / (k["total_ms"] * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
+        ns_exec = sum(kernels[k]["exec_flops"] for k in ns_kinds)
+        refresh_exec_frac = ns_exec / (T_ref * 1e-3) / (PEAK_BF16_TFLOPS * 1e12) if ref else None
+        if roofline is not None and roofline["kernel"] in ns_kinds:
+            roofline["executed_per_launch"] = kd["exec_flops"] / kd["launches"]
             roofline["executed_frac"] = roofline["executed_per_launch"] / (roofline["mean_launch_ms"] * 1e-3) / (
                 PEAK_BF16_TFLOPS * 1e12)
         rw_names = [k for k in ("rw_wide", "rw_generic", "rw_tall_stats", "rw_tall_apply") if kernels[k]["launches"]]
@@ -505,14 +486,14 @@ def main():
         "rowwise_ms": T_rw,
         "refresh_alg_tflops_frac": refresh_alg_frac,
         "refresh_executed_mfma_frac": refresh_exec_frac,
-        "refresh_executed_tflop": ns_exec / 1e12,
+        "refresh_executed_tflop": ns_exec / 1e12 if ns_exec else None,
         "gemm_executed_mfma_frac": gemm_exec_frac,
         "rowwise_hbm_frac": rowwise_hbm_frac,
         "peaks_measured": peaks,
         "refresh_alg_tflops_frac_of_measured": (ns_flops / (T_ref * 1e-3) / (peaks["mfma_bf16_tflops"] * 1e12)
                                                 if ref and peaks else None),
         "refresh_executed_mfma_frac_of_measured": (ns_exec / (T_ref * 1e-3) / (peaks["mfma_bf16_tflops"] * 1e12)
-                                                   if ref and peaks else None),
+                                                   if ref and peaks and ns_exec else None),
         "rowwise_hbm_frac_of_measured": (rw_bytes / (T_rw * 1e-3) / (peaks["hbm_rowwise_mix_gbs"] * 1e9)
                                          if rw and peaks else None),
         "amortized_ms_by_K": ({str(k): (T_ref + (k - 1) * T_rw) / k for k in (1, 3, 5, 10)}

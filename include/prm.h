@@ -87,8 +87,10 @@ typedef struct prm_config {
   int32_t grad_dtype;    /* prm_dtype of G */
   int32_t never_refresh; /* ablation: RowNorm on every step (K ignored) */
   int32_t gamma_on_refresh; /* ablation: gamma also scales the NS5 direction */
-  int32_t reserved;
-  uint64_t workspace_budget_bytes; /* NS5 workspace cap; 0 = automatic */
+  int32_t ns_plain;      /* 0 (default): matrices with c >= 2r (oriented) evaluate NS5
+                            through the factored form described at prm_step; 1: the
+                            five iterations as written for every matrix */
+  uint64_t workspace_budget_bytes; /* NS5 workspace cap; 0 = automatic (48 GiB) */
 } prm_config;
 
 typedef struct prm_ctx prm_ctx; /* opaque */
@@ -115,7 +117,16 @@ int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* 
 /* One optimizer step t (0-based, >= 0) over every matrix: the body of the
  * loop over t in Alg. 1 (momentum update, rho_t of eq. periodic-direction,
  * NS5 refresh or gamma RowNorm, shape scale, decoupled weight decay and the
- * parameter write), enqueued on the context's stream.  params[i]: W (param_dtype), grads[i]: G (grad_dtype),
+ * parameter write), enqueued on the context's stream.
+ * NS5 (eq. app-ns-recurrence) is evaluated in one of two exact forms.  For a
+ * matrix whose oriented shape has c >= 2r (unless cfg.ns_plain): every B_j
+ * is a polynomial in A_0, so the factors P_j = aI + B_j commute, and the
+ * step computes X_2 = (P_1 P_0) X_0, A_1 = P_0^2 A_0, A_3 = P_2^2 A_2,
+ * A_4 = P_3^2 A_3 and X_5 = (P_4 P_3 P_2) X_2 with r x r products, forming
+ * the Gram matrix X X^T only at j = 0 and 2 (4 r^2 c + 14 r^3 multiply-adds
+ * instead of 10 r^2 c + 5 r^3, and two bf16 roundings of the iterate instead
+ * of five).  Square and nearly square matrices run the five iterations.
+ * params[i]: W (param_dtype), grads[i]: G (grad_dtype),
  * momentum[i]: M (fp32); all device pointers, 16-byte aligned.  lr < 0 uses
  * cfg->lr.  *did_refresh (nullable) receives rho_t, computed on the host.
  * Runs on the device the context was created on; the caller's current device
@@ -159,17 +170,22 @@ int prm_plan_workspace_bytes(int32_t n_mats, const int64_t* rows, const int64_t*
  * class, the launch count, total GPU milliseconds, and the algorithmic bytes
  * and FLOPs of those launches, then clears the counters.  Classes, in order:
  * rw_wide, rw_generic, rw_tall_stats, rw_tall_finalize, rw_tall_apply,
- * ns_prologue, ns_alpha, ns_gram, ns_poly, ns_apply.  Algorithmic bytes count
- * each element of G, M and W once per read or write the method needs (the
- * tall-matrix re-read of M is not counted); algorithmic FLOPs are the paper's
- * 2r^2c (Gram), 2r^3 (square) and 2r^2c (apply) per matrix and iteration. */
-#define PRM_NUM_KERNEL_CLASSES 10
+ * ns_prologue, ns_alpha, ns_gram, ns_poly, ns_apply, ns_sprod.  Algorithmic
+ * bytes count each element of G, M and W once per read or write the method
+ * needs (the tall-matrix re-read of M is not counted).  Algorithmic FLOPs are
+ * 2 x the multiply-adds of the product a launch forms, per matrix: 2r^2c
+ * (Gram, apply: r x r times r x c), 2r^3 (square, and the r x r split
+ * products of the factored form).  Executed FLOPs are what the matrix cores
+ * actually run: padded 256 x 256 tiles, only the upper tiles of symmetric
+ * results, and the diagonal-term MFMAs of the apply. */
+#define PRM_NUM_KERNEL_CLASSES 11
 typedef struct prm_kernel_stats {
   char name[32];
   int64_t launches;
   double total_ms;
   double alg_bytes;
   double alg_flops;
+  double exec_flops;
 } prm_kernel_stats;
 int prm_profile_enable(prm_ctx* ctx, int32_t enable);
 int prm_profile_read(prm_ctx* ctx, prm_kernel_stats* out, int32_t n);

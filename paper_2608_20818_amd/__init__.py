@@ -23,10 +23,10 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libprm.so")
 PRM_OK, PRM_EINVAL, PRM_EDTYPE, PRM_EALIGN, PRM_ENOMEM, PRM_EHIP = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
 SCALE_ONE, SCALE_SQRT_ASPECT, SCALE_RMS_0P2 = 0, 1, 2
-NUM_KERNEL_CLASSES = 10
+NUM_KERNEL_CLASSES = 11
 NOALLOC_SCRATCH_BYTES = 256 << 20  # PRM_NOALLOC_SCRATCH_BYTES
 KERNEL_CLASSES = ("rw_wide", "rw_generic", "rw_tall_stats", "rw_tall_finalize", "rw_tall_apply",
-                  "ns_prologue", "ns_alpha", "ns_gram", "ns_poly", "ns_apply")
+                  "ns_prologue", "ns_alpha", "ns_gram", "ns_poly", "ns_apply", "ns_sprod")
 
 
 class PRMError(RuntimeError):
@@ -43,7 +43,7 @@ class Config(ctypes.Structure):
         ("ns_c", ctypes.c_float), ("nesterov", ctypes.c_int32), ("ema_dampening", ctypes.c_int32),
         ("scale_mode", ctypes.c_int32), ("param_dtype", ctypes.c_int32),
         ("grad_dtype", ctypes.c_int32), ("never_refresh", ctypes.c_int32),
-        ("gamma_on_refresh", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("gamma_on_refresh", ctypes.c_int32), ("ns_plain", ctypes.c_int32),
         ("workspace_budget_bytes", ctypes.c_uint64),
     ]
 
@@ -59,7 +59,7 @@ class AdamWConfig(ctypes.Structure):
 class KernelStats(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int64),
                 ("total_ms", ctypes.c_double), ("alg_bytes", ctypes.c_double),
-                ("alg_flops", ctypes.c_double)]
+                ("alg_flops", ctypes.c_double), ("exec_flops", ctypes.c_double)]
 
 
 _lib = None
@@ -278,8 +278,8 @@ class Optimizer:
     def profile_read(self) -> dict:
         out = (KernelStats * NUM_KERNEL_CLASSES)()
         _check(load().prm_profile_read(self._ctx, out, NUM_KERNEL_CLASSES))
-        return {o.name.decode(): {"launches": o.launches, "total_ms": o.total_ms,
-                                  "alg_bytes": o.alg_bytes, "alg_flops": o.alg_flops} for o in out}
+        return {o.name.decode(): {"launches": o.launches, "total_ms": o.total_ms, "alg_bytes": o.alg_bytes,
+                                  "alg_flops": o.alg_flops, "exec_flops": o.exec_flops} for o in out}
 
     def close(self):
         if getattr(self, "_ctx", None) is not None and self._ctx.value:

@@ -20,12 +20,22 @@
 //                                      with transposing ds_read_b64_tr_b16;
 //                                      upper tiles only, mirrored
 //      square A^2 = A A^T              (A is symmetric) upper tiles, mirrored
+//      split  C = X Y                  product of two commuting symmetric
+//                                      matrices (C symmetric), upper tiles, mirrored
 //      apply  X'^T = XT (aI + dB) + XT Bo    ("NT"; Bo is symmetric)
-//    The diagonals of A and B are the large entries, so they are carried in
-//    fp32 and only the off-diagonal parts Ao, Bo are rounded to bf16 for the
-//    next product:  A^2 = dA^2 + dA Ao + Ao dA + Ao Ao, with the diagonal terms
-//    applied in the epilogues.  Epilogues also fold alpha, and at the last
-//    iteration perform the parameter write W <- (1 - eta lambda) W - eta s O^{-1}(X_5).
+//    The diagonals of these symmetric matrices are the large entries, so they
+//    are carried in fp32 and only the off-diagonal parts (Ao, Bo, ...) are
+//    rounded to bf16 for the next product:  A^2 = dA^2 + dA Ao + Ao dA + Ao Ao,
+//    with the diagonal terms applied in the epilogues.  Epilogues also fold
+//    alpha, and the last apply performs the parameter write
+//    W <- (1 - eta lambda) W - eta s O^{-1}(X_5).
+//
+// Which matrices play which role, and in what order the kinds run, is the
+// dispatcher's choice (prm_api.hip): either the five iterations as written,
+// or, for wide oriented shapes, the same map evaluated with r x r products
+// between two explicit iterates (every B_j is a polynomial in A_0, so the
+// factors aI + B_j commute: X_2 = P_1 P_0 X_0, A_{j+1} = P_j^2 A_j,
+// X_5 = P_4 P_3 P_2 X_2).
 // The workspace is padded to whole tiles and the padding stays exactly zero
 // through every iteration, so the GEMMs need no bounds checks.
 #include <type_traits>
@@ -210,9 +220,8 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  const bool even = (p.iter & 1) == 0;
-  const uint16_t* XTc = even ? d.XT : d.XTn;
-  uint16_t* XTo = even ? d.XTn : d.XT;
+  const uint16_t* XTc = p.src == 0 ? d.XT : d.XTn;
+  uint16_t* XTo = p.src == 0 ? d.XTn : d.XT;
   const int64_t rp = d.rp, cp = d.cp;
 
   // C[row][col] = sum_k P[row][k] Q[col][k]   (NT), or
@@ -224,9 +233,11 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   if constexpr (KIND == GEMM_GRAM) {
     P = XTc; Q = XTc; klen = cp;
   } else if constexpr (KIND == GEMM_POLY) {
-    P = d.Ao; Q = d.Ao; klen = rp;
+    P = d.S[p.sx]; Q = P; klen = rp;   // Ao Ao (Ao is symmetric)
+  } else if constexpr (KIND == GEMM_SPROD) {
+    P = d.S[p.sx]; Q = d.S[p.sy]; klen = rp;   // Xo Yo (Yo is symmetric)
   } else {
-    P = XTc; Q = d.Bo; klen = rp;   // X'^T tile: rows of XT, columns of Bo
+    P = XTc; Q = d.S[p.sy]; klen = rp;   // X'^T tile: rows of XT, columns of the factor
   }
   const int64_t row0 = (int64_t)it.tm * BM, col0 = (int64_t)it.tn * BN;
   const int nk = (int)(klen / BK);  // a multiple of 4: the padded dimensions are multiples of the tile
@@ -329,7 +340,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   if constexpr (KIND == GEMM_APPLY) {
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
-      const float v = p.a + d.dB[col0 + wn * WN + 32 * j + (lane & 31)];
+      const float v = p.yshift + d.dS[p.sy][col0 + wn * WN + 32 * j + (lane & 31)];
       fold_hi[j] = f2bf(v);
       fold_lo[j] = f2bf(v - bf2f(fold_hi[j]));
     }
@@ -511,21 +522,22 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // Lane L holds output row 32 i + L % 32 of its wave block and, for block
   // column j and q = 0..3, the 4 columns 32 j + 8 q + 4 (L / 32) + 0..3.
   const bool diag = (KIND != GEMM_APPLY) && it.tm == it.tn;  // Gram / square tile on the diagonal
-  if constexpr (KIND == GEMM_POLY) {
-    // the square needs the Ao tile of its own output position: it enters the
-    // staging area (layout below) by 1 KB DMA wave loads, 2 tile rows each,
-    // and every lane later reads and overwrites its own 8 bytes in place
+  if constexpr (KIND == GEMM_POLY || KIND == GEMM_SPROD) {
+    // the square (split product) needs the tile of its (first) operand at its
+    // own output position: it enters the staging area (layout below) by 1 KB
+    // DMA wave loads, 2 tile rows each, and every lane later reads and
+    // overwrites its own 8 bytes in place
 #pragma unroll 4
     for (int q = 0; q < BM / 2 / NWAVES; ++q) {
       const int r2 = 2 * ((BM / 2 / NWAVES) * wave + q);  // first row of the pair (even)
       const int R = r2 + (lane >> 5);
       const int c = (lane & 31) ^ (R & 31);
-      __builtin_amdgcn_global_load_lds((const void*)(d.Ao + (row0 + R) * rp + col0 + 8 * c),
+      __builtin_amdgcn_global_load_lds((const void*)(d.S[p.sx] + (row0 + R) * rp + col0 + 8 * c),
                                        (lds_ptr)((r2 < 128 ? s0 : s1) + (r2 & 127) * 512), 16, 0, 0);
     }
     __syncthreads();
   }
-  const float alpha = (p.iter == 0) ? *d.alpha : 1.0f;
+  const float alpha = p.use_alpha ? *d.alpha : 1.0f;
   const bool last = (KIND == GEMM_APPLY) && p.last;
   {
     const float s2 = alpha * alpha;
@@ -535,22 +547,34 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     // == L / 32, at q = (L % 32) / 8, element (L % 32) % 4
     const bool dlane = diag && wm == wn && ((m >> 2) & 1) == hl;
     const int64_t grow = row0 + wm * WM + m, gcol = col0 + wn * WN + 4 * hl;
-    float* dout = (KIND == GEMM_GRAM) ? d.dA : d.dB;
-    // square: dA of this lane's columns (the same for every row block)
+    float* dout = d.dS[p.so];
+    // square / split product: diagonal of the (second) operand at this lane's
+    // columns (the same for every row block), shift included
+    constexpr bool SPLIT = KIND == GEMM_POLY || KIND == GEMM_SPROD;
+    const float* dX = d.dS[p.sx];
+    const float* dY = (KIND == GEMM_SPROD) ? d.dS[p.sy] : dX;
+    const float ys = (KIND == GEMM_SPROD) ? p.yshift : p.xshift;
+    const uint16_t* Yo = d.S[p.sy];
+    const bool same = p.sx == p.sy;  // split product of a matrix with itself: Yo tile = staged Xo tile
     float dcol[NI][4][4];
-    if constexpr (KIND == GEMM_POLY) {
+    if constexpr (SPLIT) {
 #pragma unroll
       for (int j = 0; j < NI; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) Vec<float>::load4(d.dA + gcol + 32 * j + 8 * q, dcol[j][q]);
+        for (int q = 0; q < 4; ++q) {
+          Vec<float>::load4(dY + gcol + 32 * j + 8 * q, dcol[j][q]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dcol[j][q][e] += ys;
+        }
     }
 #pragma unroll
     for (int ih = 0; ih < MI; ih += 2) {
-      // square: dA of rows 32 i + L % 32 for two row blocks
+      // square / split product: diagonal of the first operand at rows
+      // 32 i + L % 32 for two row blocks, shift included
       float drow[2];
-      if constexpr (KIND == GEMM_POLY) {
+      if constexpr (SPLIT) {
 #pragma unroll
-        for (int ii = 0; ii < 2; ++ii) drow[ii] = d.dA[grow + 32 * (ih + ii)];
+        for (int ii = 0; ii < 2; ++ii) drow[ii] = dX[grow + 32 * (ih + ii)] + p.xshift;
       }
 #pragma unroll
       for (int ii = 0; ii < 2; ++ii) {
@@ -574,6 +598,16 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
 #pragma unroll
               for (int e = 0; e < 4; ++e)
                 v[e] = p.c * acc[i][j][4 * q + e] + (p.b + p.c * (drow[ii] + dcol[j][q][e])) * a4[e];
+            } else if constexpr (KIND == GEMM_SPROD) {
+              // (dX + Xo)(dY + Yo) = Xo Yo + dX Yo + Xo dY (+ dX dY on the diagonal)
+              const int ch0 = (wn * WN + 32 * j + 8 * q) >> 3;
+              const uint2 w2 = *reinterpret_cast<const uint2*>(trow + ((ch0 ^ (r & 31)) << 4));
+              const float a4[4] = {bf2f(w2.x & 0xffffu), bf2f(w2.x >> 16), bf2f(w2.y & 0xffffu), bf2f(w2.y >> 16)};
+              float y4[4] = {a4[0], a4[1], a4[2], a4[3]};
+              if (!same) Vec<uint16_t>::load4(Yo + (grow + 32 * i) * rp + gcol + 32 * j + 8 * q, y4);
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                v[e] = acc[i][j][4 * q + e] + drow[ii] * y4[e] + a4[e] * dcol[j][q][e];
             } else {
               // X'^T = alpha (XT diag(a + dB) + XT Bo); both terms are in acc
 #pragma unroll
@@ -586,7 +620,13 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
 #pragma unroll
                 for (int e = 1; e < 4; ++e) dv = (e == (m & 3)) ? acc[i][j][4 * q + e] : dv;
                 if constexpr (KIND == GEMM_GRAM) dv = s2 * dv;
-                else dv = p.b * drow[ii] + p.c * (dv + drow[ii] * drow[ii]);
+                else if constexpr (KIND == GEMM_POLY) dv = p.b * drow[ii] + p.c * (dv + drow[ii] * drow[ii]);
+                else {
+                  float dd = dcol[j][q][0];
+#pragma unroll
+                  for (int e = 1; e < 4; ++e) dd = (e == (m & 3)) ? dcol[j][q][e] : dd;
+                  dv = dv + drow[ii] * dd;
+                }
                 dout[grow + 32 * i] = dv;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) v[e] = (e == (m & 3)) ? 0.f : v[e];
@@ -636,7 +676,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
       }
     }
   };
-  uint16_t* const out = (KIND == GEMM_GRAM) ? d.Ao : (KIND == GEMM_POLY) ? d.Bo : XTo;
+  uint16_t* const out = (KIND == GEMM_APPLY) ? XTo : d.S[p.so];
   if (!last || d.tall) {
     const int ch = tid & 31;
     constexpr int ROWS_PER_IT = NTHREADS / 32;
@@ -696,6 +736,7 @@ hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item
   switch (kind) {
     case GEMM_GRAM: ns_gemm_kernel<GEMM_GRAM, BF16><<<g, b, 0, s>>>(md, items, p); break;
     case GEMM_POLY: ns_gemm_kernel<GEMM_POLY, BF16><<<g, b, 0, s>>>(md, items, p); break;
+    case GEMM_SPROD: ns_gemm_kernel<GEMM_SPROD, BF16><<<g, b, 0, s>>>(md, items, p); break;
     case GEMM_APPLY:
       if (wt == BF16) ns_gemm_kernel<GEMM_APPLY, BF16><<<g, b, 0, s>>>(md, items, p);
       else ns_gemm_kernel<GEMM_APPLY, F32><<<g, b, 0, s>>>(md, items, p);

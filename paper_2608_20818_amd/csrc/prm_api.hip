@@ -44,7 +44,7 @@ int fail(int code, const char* fmt, ...) {
       return fail(PRM_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));              \
   } while (0)
 
-constexpr uint64_t kAutoBudget = 32ull << 30;  // NS5 chunk workspace cap when unset
+constexpr uint64_t kAutoBudget = 48ull << 30;  // NS5 chunk workspace cap when unset
 constexpr int64_t kMaxDim = 1ll << 24;
 
 // Makes the context's device current for one entry point and restores the
@@ -87,12 +87,12 @@ inline uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
 
 enum KClass {
   K_RW_WIDE = 0, K_RW_GENERIC, K_RW_TALL_STATS, K_RW_TALL_FIN, K_RW_TALL_APPLY,
-  K_NS_PROLOGUE, K_NS_ALPHA, K_NS_GRAM, K_NS_POLY, K_NS_APPLY, K_NCLASS
+  K_NS_PROLOGUE, K_NS_ALPHA, K_NS_GRAM, K_NS_POLY, K_NS_APPLY, K_NS_SPROD, K_NCLASS
 };
 static_assert(K_NCLASS == PRM_NUM_KERNEL_CLASSES, "kernel class table");
 const char* kClassName[K_NCLASS] = {"rw_wide", "rw_generic", "rw_tall_stats",
                                     "rw_tall_finalize", "rw_tall_apply", "ns_prologue",
-                                    "ns_alpha", "ns_gram", "ns_poly", "ns_apply"};
+                                    "ns_alpha", "ns_gram", "ns_poly", "ns_apply", "ns_sprod"};
 
 struct WideClass {
   int tpr, nch;
@@ -102,17 +102,31 @@ struct WideClass {
   double elems = 0;
 };
 
+// The matrices of a chunk that run the same NS5 sequence, with their tile
+// lists: `upper` for the symmetric r x r results (Gram, square, split
+// products), `apply` for the tiles of X'^T.  Per launch over the group:
+// algorithmic FLOPs of an r x r times r x c product (Gram, apply) and of an
+// r x r product, and the executed FLOPs of each kind.
+struct NsGroup {
+  std::vector<int32_t> mats;
+  std::vector<Item> upper, apply;
+  size_t off_upper = 0, off_apply = 0;
+  double elems = 0, alg_rc = 0, alg_rr = 0, exec_gram = 0, exec_rr = 0, exec_apply = 0;
+};
+
 struct Chunk {
   std::vector<int32_t> mats;
-  std::vector<Item> prologue, gram, poly, apply;
-  size_t off_mats = 0, off_prologue = 0, off_gram = 0, off_poly = 0, off_apply = 0;
-  double elems = 0, flops_gram = 0, flops_poly = 0, flops_apply = 0;
+  std::vector<Item> prologue;
+  size_t off_mats = 0, off_prologue = 0;
+  double elems = 0;
+  NsGroup plain, chain;  // five iterations as written; the factored form
 };
 
 struct Plan {
   int32_t n = 0;
   std::vector<int64_t> m, nn, rp, cp;
   std::vector<int32_t> tall;
+  std::vector<int32_t> chain;       // NS5 in the factored form (oriented c >= 2r)
   std::vector<float> s;
   std::vector<uint64_t> ws_off;     // offset of the matrix's NS region inside the chunk area
   std::vector<uint64_t> small_off;  // partial sums + alpha
@@ -145,6 +159,7 @@ int validate_cfg(const prm_config* c) {
   if (c->ema_dampening != 0 && c->ema_dampening != 1) return fail(PRM_EINVAL, "ema_dampening must be 0 or 1");
   if (c->never_refresh != 0 && c->never_refresh != 1) return fail(PRM_EINVAL, "never_refresh must be 0 or 1");
   if (c->gamma_on_refresh != 0 && c->gamma_on_refresh != 1) return fail(PRM_EINVAL, "gamma_on_refresh must be 0 or 1");
+  if (c->ns_plain != 0 && c->ns_plain != 1) return fail(PRM_EINVAL, "ns_plain must be 0 or 1");
   if (c->scale_mode < 0 || c->scale_mode > 2) return fail(PRM_EINVAL, "unknown scale_mode %d", c->scale_mode);
   if (c->param_dtype != PRM_F32 && c->param_dtype != PRM_BF16) return fail(PRM_EDTYPE, "unsupported param_dtype %d", c->param_dtype);
   if (c->grad_dtype != PRM_F32 && c->grad_dtype != PRM_BF16) return fail(PRM_EDTYPE, "unsupported grad_dtype %d", c->grad_dtype);
@@ -160,11 +175,13 @@ float shape_scale(int64_t m, int64_t n, int mode) {
 }
 
 // NS5 workspace of one matrix: the transposed iterate and the next one (bf16),
-// off-diagonal A and B (bf16), diagonals of A and B (fp32).
-uint64_t ns_matrix_bytes(int64_t rp, int64_t cp) {
+// and the split symmetric r x r matrices (bf16 off-diagonal part, fp32
+// diagonal): two on the plain path (A, B), four on the factored one.
+int ns_splits(int chain) { return chain ? 4 : 2; }
+uint64_t ns_matrix_bytes(int64_t rp, int64_t cp, int chain) {
   const uint64_t xs = align256((uint64_t)rp * cp * 2), gs = align256((uint64_t)rp * rp * 2),
                  vs = align256((uint64_t)rp * 4);
-  return 2 * xs + 2 * gs + 2 * vs;
+  return 2 * xs + (uint64_t)ns_splits(chain) * (gs + vs);
 }
 
 // Row-wise launch class of a wide row of length n (0 tpr = generic path).
@@ -194,6 +211,9 @@ int make_plan(int32_t n_mats, const int64_t* rows, const int64_t* cols, const pr
     P.m.push_back(m);
     P.nn.push_back(n);
     P.tall.push_back(m > n ? 1 : 0);
+    // the factored form needs c >= 2r: it saves work only there, and its
+    // rounding stays below the plain path's only away from square shapes
+    P.chain.push_back(!cfg->ns_plain && c >= 2 * r ? 1 : 0);
     P.rp.push_back(round_up(r, kNsTile));
     P.cp.push_back(round_up(c, kNsTile));
     P.s.push_back(shape_scale(m, n, cfg->scale_mode));
@@ -230,7 +250,7 @@ int make_plan(int32_t n_mats, const int64_t* rows, const int64_t* cols, const pr
   P.ws_off.assign(n_mats, 0);
   uint64_t cur = 0;
   for (int idx : order) {
-    const uint64_t need = ns_matrix_bytes(P.rp[idx], P.cp[idx]);
+    const uint64_t need = ns_matrix_bytes(P.rp[idx], P.cp[idx], P.chain[idx]);
     if (need > budget)
       return fail(PRM_ENOMEM, "matrix %d needs %llu workspace bytes, budget is %llu", idx,
                   (unsigned long long)need, (unsigned long long)budget);
@@ -319,37 +339,47 @@ void build_lists(Plan& P, const prm_config* cfg) {
     (vec == 4 ? P.tall_elems4 : P.tall_elems1) += (double)P.m[i] * P.nn[i];
     for (int32_t cb = 0; cb < (P.nn[i] + 255) / 256; ++cb) P.fin_items.push_back(Item{i, 0, cb, 0});
   }
-  // NS5 lists per chunk
+  // NS5 lists per chunk and group
   for (auto& ch : P.chunks) {
     for (int i : ch.mats) {
       const int64_t pm = (P.tall[i] ? P.cp[i] : P.rp[i]) / kPrologueTile;
       const int64_t pn = (P.tall[i] ? P.rp[i] : P.cp[i]) / kPrologueTile;
       for (int32_t a = 0; a < pm; ++a)
         for (int32_t b = 0; b < pn; ++b) ch.prologue.push_back(Item{i, a, b, 0});
-      const double r = (double)std::min(P.m[i], P.nn[i]), c = (double)std::max(P.m[i], P.nn[i]);
-      ch.elems += r * c;
-      ch.flops_gram += 2 * r * r * c;
-      ch.flops_poly += 2 * r * r * r;
-      ch.flops_apply += 2 * r * r * c;
+      ch.elems += (double)P.m[i] * P.nn[i];
     }
-    std::vector<std::vector<Item>> g(kXcds), a(kXcds);
-    for (size_t k = 0; k < ch.mats.size(); ++k) {
-      const int i = ch.mats[k];
-      const int32_t tr = (int32_t)(P.rp[i] / kNsTile), tc = (int32_t)(P.cp[i] / kNsTile);
-      // Gram and square: each matrix's (upper) tiles stay on one XCD, whose 32
-      // CUs then share its r x r panels in their L2
-      tile_order(i, tr, tr, true, g[k % kXcds]);
-      // apply: every XCD takes a contiguous eighth of each matrix's tile order,
-      // so all XCDs stream the same Bo at the same time (it is read by every
-      // tile row; the last-level cache then serves the repeats)
-      std::vector<Item> ta;
-      tile_order(i, tc, tr, false, ta);  // tiles of X'^T: rows over c, columns over r
-      for (int x = 0; x < kXcds; ++x)
-        a[x].insert(a[x].end(), ta.begin() + ta.size() * x / kXcds, ta.begin() + ta.size() * (x + 1) / kXcds);
+    for (int grp = 0; grp < 2; ++grp) {
+      NsGroup& G = grp ? ch.chain : ch.plain;
+      std::vector<std::vector<Item>> u(kXcds), a(kXcds);
+      for (int i : ch.mats) {
+        if (P.chain[i] != grp) continue;
+        const size_t k = G.mats.size();
+        G.mats.push_back(i);
+        const double r = (double)std::min(P.m[i], P.nn[i]), c = (double)std::max(P.m[i], P.nn[i]);
+        const double rp = (double)P.rp[i], cp = (double)P.cp[i], t2 = (double)kNsTile * kNsTile;
+        const int32_t tr = (int32_t)(P.rp[i] / kNsTile), tc = (int32_t)(P.cp[i] / kNsTile);
+        const double upper = (double)tr * (tr + 1) / 2;
+        G.elems += r * c;
+        G.alg_rc += 2 * r * r * c;
+        G.alg_rr += 2 * r * r * r;
+        G.exec_gram += upper * 2 * t2 * cp;
+        G.exec_rr += upper * 2 * t2 * rp;
+        // the apply's diagonal term adds 64 MFMAs per wave to 64 per stage
+        G.exec_apply += (double)tc * tr * 2 * t2 * rp * (1.0 + kNsTile / 4.0 / rp);
+        // symmetric products: each matrix's (upper) tiles stay on one XCD,
+        // whose 32 CUs then share its r x r panels in their L2
+        tile_order(i, tr, tr, true, u[k % kXcds]);
+        // apply: every XCD takes a contiguous eighth of each matrix's tile
+        // order, so all XCDs stream the same factor at the same time (it is
+        // read by every tile row; the last-level cache serves the repeats)
+        std::vector<Item> ta;
+        tile_order(i, tc, tr, false, ta);  // tiles of X'^T: rows over c, columns over r
+        for (int x = 0; x < kXcds; ++x)
+          a[x].insert(a[x].end(), ta.begin() + ta.size() * x / kXcds, ta.begin() + ta.size() * (x + 1) / kXcds);
+      }
+      G.upper = interleave_xcd(u);
+      G.apply = interleave_xcd(a);
     }
-    ch.gram = interleave_xcd(g);
-    ch.poly = ch.gram;
-    ch.apply = interleave_xcd(a);
   }
   (void)cfg;
   // flatten
@@ -375,9 +405,10 @@ void build_lists(Plan& P, const prm_config* cfg) {
   for (auto& ch : P.chunks) {
     ch.off_mats = put_ints(ch.mats);
     ch.off_prologue = put_items(ch.prologue);
-    ch.off_gram = put_items(ch.gram);
-    ch.off_poly = put_items(ch.poly);
-    ch.off_apply = put_items(ch.apply);
+    for (NsGroup* G : {&ch.plain, &ch.chain}) {
+      G->off_upper = put_items(G->upper);
+      G->off_apply = put_items(G->apply);
+    }
   }
   if (P.ints.empty()) P.ints.push_back(0);
   if (P.items.empty()) P.items.push_back(Item{0, 0, 0, 0});
@@ -401,10 +432,11 @@ void fill_descs(const Plan& P, char* chunk_base, char* small_base, char* tall_ba
     char* w = chunk_base + P.ws_off[i];
     d.XT = (uint16_t*)w;
     d.XTn = (uint16_t*)(w + xs);
-    d.Ao = (uint16_t*)(w + 2 * xs);
-    d.Bo = (uint16_t*)(w + 2 * xs + gs);
-    d.dA = (float*)(w + 2 * xs + 2 * gs);
-    d.dB = (float*)(w + 2 * xs + 2 * gs + vs);
+    const int ns = ns_splits(P.chain[i]);
+    for (int k = 0; k < 4; ++k) {
+      d.S[k] = k < ns ? (uint16_t*)(w + 2 * xs + k * gs) : nullptr;
+      d.dS[k] = k < ns ? (float*)(w + 2 * xs + ns * gs + k * vs) : nullptr;
+    }
     d.ptiles_m = (int32_t)((d.tall ? d.cp : d.rp) / kPrologueTile);
     d.ptiles_n = (int32_t)((d.tall ? d.rp : d.cp) / kPrologueTile);
     d.partial = (float*)(small_base + P.small_off[i]);
@@ -420,7 +452,7 @@ void fill_descs(const Plan& P, char* chunk_base, char* small_base, char* tall_ba
 struct ProfRec {
   int cls;
   hipEvent_t e0, e1;
-  double bytes, flops;
+  double bytes, flops, exec;
 };
 
 }  // namespace
@@ -460,7 +492,7 @@ hipEvent_t take_event(prm_ctx* c) {
 
 // Run `launch` on the context stream, bracketed by events when profiling.
 template <typename F>
-int timed(prm_ctx* c, int cls, double bytes, double flops, F&& launch) {
+int timed(prm_ctx* c, int cls, double bytes, double flops, F&& launch, double exec = 0) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (c->prof) {
     e0 = take_event(c);
@@ -472,7 +504,7 @@ int timed(prm_ctx* c, int cls, double bytes, double flops, F&& launch) {
   if (e != hipSuccess) return fail(PRM_EHIP, "%s launch failed: %s", kClassName[cls], hipGetErrorString(e));
   if (c->prof) {
     HIP_TRY(hipEventRecord(e1, c->stream));
-    c->recs.push_back(ProfRec{cls, e0, e1, bytes, flops});
+    c->recs.push_back(ProfRec{cls, e0, e1, bytes, flops, exec});
   }
   return PRM_OK;
 }
@@ -574,6 +606,7 @@ int refresh_step(prm_ctx* c, float lr, bool debug) {
   const Plan& P = c->plan;
   const prm_config& cf = c->cfg;
   NsParams p;
+  std::memset(&p, 0, sizeof(p));
   p.beta = cf.beta;
   p.gcoef = cf.ema_dampening ? 1.0f - cf.beta : 1.0f;
   p.nesterov = cf.nesterov;
@@ -588,11 +621,9 @@ int refresh_step(prm_ctx* c, float lr, bool debug) {
   const DType wt = (DType)cf.param_dtype, gt = (DType)cf.grad_dtype;
   const double gb = gt == BF16 ? 2 : 4, wb = wt == BF16 ? 2 : 4, db = debug ? 4 : 0;
   const MatDesc* md = c->d_desc;
-  constexpr int kIters = 5;
+  const float a = cf.ns_a;
   int rc;
   for (const auto& ch : P.chunks) {
-    p.iter = 0;
-    p.last = 0;
     rc = timed(c, K_NS_PROLOGUE, ch.elems * (gb + 8 + 2), 0, [&] {  // G, M read; M, bf16 X^T written
       return launch_ns_prologue(gt, md, c->d_items + ch.off_prologue, (int32_t)ch.prologue.size(), p, c->stream);
     });
@@ -601,21 +632,66 @@ int refresh_step(prm_ctx* c, float lr, bool debug) {
       return launch_ns_alpha(md, c->d_ints + ch.off_mats, (int32_t)ch.mats.size(), p, c->stream);
     });
     if (rc) return rc;
-    for (int j = 0; j < kIters; ++j) {
-      p.iter = j;
-      p.last = (j == kIters - 1) ? 1 : 0;
-      rc = timed(c, K_NS_GRAM, 0, ch.flops_gram, [&] {
-        return launch_ns_gemm(GEMM_GRAM, wt, md, c->d_items + ch.off_gram, (int32_t)ch.gram.size(), p, c->stream);
-      });
-      if (rc) return rc;
-      rc = timed(c, K_NS_POLY, 0, ch.flops_poly, [&] {
-        return launch_ns_gemm(GEMM_POLY, wt, md, c->d_items + ch.off_poly, (int32_t)ch.poly.size(), p, c->stream);
-      });
-      if (rc) return rc;
-      rc = timed(c, K_NS_APPLY, p.last ? ch.elems * (2 * wb + db) : 0, ch.flops_apply, [&] {
-        return launch_ns_gemm(GEMM_APPLY, wt, md, c->d_items + ch.off_apply, (int32_t)ch.apply.size(), p, c->stream);
-      });
-      if (rc) return rc;
+    for (const NsGroup* Gp : {&ch.plain, &ch.chain}) {
+      const NsGroup& G = *Gp;
+      if (G.mats.empty()) continue;
+      const Item* upper = c->d_items + G.off_upper;
+      const Item* apply = c->d_items + G.off_apply;
+      const int32_t nu = (int32_t)G.upper.size(), na = (int32_t)G.apply.size();
+      // one kernel of the sequence: Gram of the iterate `src` into S[so];
+      // B = bA + cA^2 from S[sx] into S[so]; the split product
+      // (S[sx] + xs I)(S[sy] + ys I) into S[so]; the apply of (S[sy] + ys I)
+      // to the iterate `src`, into the other iterate or, `last`, into W
+      auto gram = [&](int src, int alpha, int so) {
+        p.src = src; p.use_alpha = alpha; p.so = so;
+        return timed(c, K_NS_GRAM, 0, G.alg_rc, [&] {
+          return launch_ns_gemm(GEMM_GRAM, wt, md, upper, nu, p, c->stream);
+        }, G.exec_gram);
+      };
+      auto poly = [&](int sx, int so) {
+        p.sx = sx; p.sy = sx; p.so = so; p.xshift = 0.f; p.yshift = 0.f;
+        return timed(c, K_NS_POLY, 0, G.alg_rr, [&] {
+          return launch_ns_gemm(GEMM_POLY, wt, md, upper, nu, p, c->stream);
+        }, G.exec_rr);
+      };
+      auto sprod = [&](int sx, float xs, int sy, float ys, int so) {
+        p.sx = sx; p.sy = sy; p.so = so; p.xshift = xs; p.yshift = ys;
+        return timed(c, K_NS_SPROD, 0, G.alg_rr, [&] {
+          return launch_ns_gemm(GEMM_SPROD, wt, md, upper, nu, p, c->stream);
+        }, G.exec_rr);
+      };
+      auto applyk = [&](int src, int alpha, int sy, float ys, int last) {
+        p.src = src; p.use_alpha = alpha; p.sy = sy; p.yshift = ys; p.last = last;
+        rc = timed(c, K_NS_APPLY, last ? G.elems * (2 * wb + db) : 0, G.alg_rc, [&] {
+          return launch_ns_gemm(GEMM_APPLY, wt, md, apply, na, p, c->stream);
+        }, G.exec_apply);
+        p.last = 0;
+        return rc;
+      };
+      if (Gp == &ch.plain) {
+        // eq. (app-ns-recurrence) as written: A_j = X_j X_j^T in S0, B_j in S1,
+        // X_{j+1} = (aI + B_j) X_j
+        for (int j = 0; j < 5; ++j) {
+          if ((rc = gram(j & 1, j == 0, 0)) || (rc = poly(0, 1)) || (rc = applyk(j & 1, j == 0, 1, a, j == 4)))
+            return rc;
+        }
+      } else {
+        // the factored form, with P_j = aI + B_j:
+        //   j = 0: A0 (S0) = X0 X0^T, B0 (S1)
+        //   j = 1: P0^2 (S2), A1 = P0^2 A0 (S3), B1 (S0), Q = P1 P0 (S2); X2 = Q X0
+        //   j = 2: A2 (S0) = X2 X2^T, B2 (S1)
+        //   j = 3: P2^2 (S2), A3 = P2^2 A2 (S3), B3 (S0), Q = P3 P2 (S2)
+        //   j = 4: P3^2 (S1), A4 = P3^2 A3 (S0), B4 (S1), Q = P4 Q (S3); X5 = Q X2
+        if ((rc = gram(0, 1, 0)) || (rc = poly(0, 1)) ||
+            (rc = sprod(1, a, 1, a, 2)) || (rc = sprod(2, 0.f, 0, 0.f, 3)) || (rc = poly(3, 0)) ||
+            (rc = sprod(0, a, 1, a, 2)) || (rc = applyk(0, 1, 2, 0.f, 0)) ||
+            (rc = gram(1, 0, 0)) || (rc = poly(0, 1)) ||
+            (rc = sprod(1, a, 1, a, 2)) || (rc = sprod(2, 0.f, 0, 0.f, 3)) || (rc = poly(3, 0)) ||
+            (rc = sprod(0, a, 1, a, 2)) ||
+            (rc = sprod(0, a, 0, a, 1)) || (rc = sprod(1, 0.f, 3, 0.f, 0)) || (rc = poly(0, 1)) ||
+            (rc = sprod(1, a, 2, 0.f, 3)) || (rc = applyk(1, 0, 3, 0.f, 1)))
+          return rc;
+      }
     }
   }
   return PRM_OK;
@@ -903,6 +979,7 @@ int prm_profile_read(prm_ctx* ctx, prm_kernel_stats* out, int32_t n) {
     acc[r.cls].total_ms += ms;
     acc[r.cls].alg_bytes += r.bytes;
     acc[r.cls].alg_flops += r.flops;
+    acc[r.cls].exec_flops += r.exec;
   }
   ctx->recs.clear();
   ctx->pool_used = 0;
@@ -1187,7 +1264,7 @@ int prm_step_noalloc(const prm_config* cfg, int64_t rows, int64_t cols, void* pa
   const int64_t pn = (P.tall[0] ? P.rp[0] : P.cp[0]) / kPrologueTile;
   const int64_t pm = (P.tall[0] ? P.cp[0] : P.rp[0]) / kPrologueTile;
   const int64_t slabs = (P.nn[0] + 255) / 256;
-  const int64_t nitems = rho ? pm * pn + T * (T + 1) + tc * T : (P.tall[0] ? (int64_t)P.nrb[0] * slabs + slabs : 0);
+  const int64_t nitems = rho ? pm * pn + T * (T + 1) / 2 + tc * T : (P.tall[0] ? (int64_t)P.nrb[0] * slabs + slabs : 0);
   const uint64_t off_ints = align256(sizeof(MatDesc)), off_items = off_ints + 256;
   const uint64_t off_small = off_items + align256((uint64_t)std::max<int64_t>(nitems, 1) * sizeof(Item));
   const uint64_t off_big = off_small + align256(P.small_bytes);
@@ -1214,10 +1291,10 @@ int prm_step_noalloc(const prm_config* cfg, int64_t rows, int64_t cols, void* pa
   bool ok = true;
   if (rho) {
     Chunk& ch = P.chunks[0];
+    NsGroup& G = P.chain[0] ? ch.chain : ch.plain;  // the other group is empty
     ok = add(ch.off_prologue, ch.prologue.size(), pm * pn, pn, 0) &&
-         add(ch.off_gram, ch.gram.size(), T * (T + 1) / 2, T, 1) &&
-         add(ch.off_poly, ch.poly.size(), T * (T + 1) / 2, T, 1) &&
-         add(ch.off_apply, ch.apply.size(), tc * T, T, 0);
+         add(G.off_upper, G.upper.size(), T * (T + 1) / 2, T, 1) &&
+         add(G.off_apply, G.apply.size(), tc * T, T, 0);
   } else if (P.tall[0]) {
     const bool v4 = !P.tall_items4.empty();
     ok = add(v4 ? P.off_tall4 : P.off_tall1, v4 ? P.tall_items4.size() : P.tall_items1.size(),

@@ -25,10 +25,13 @@ struct MatDesc {
   // iterate is kept transposed, XT = X^T (cp x rp, row-major).
   uint16_t* XT;   // cp x rp   iterate
   uint16_t* XTn;  // cp x rp   next iterate
-  uint16_t* Ao;   // rp x rp   Gram matrix A = X X^T with its diagonal set to zero (bf16)
-  uint16_t* Bo;   // rp x rp   B = b A + c A^2 with its diagonal set to zero (bf16)
-  float* dA;      // rp        diagonal of A (fp32)
-  float* dB;      // rp        diagonal of B (fp32)
+  // Symmetric r x r matrices in split form: S[k] (rp x rp, bf16) holds the
+  // off-diagonal part (diagonal stored as zero), dS[k] (rp, fp32) the
+  // diagonal.  The dispatcher assigns them roles (the Gram matrix A, B =
+  // bA + cA^2, and for the chained path the products of the factors aI + B);
+  // matrices on the plain five-iteration path use S[0], S[1] only.
+  uint16_t* S[4];
+  float* dS[4];
   float* partial; // prologue: one sum of squares per 64 x 64 tile
   float* alpha;   // 1 / (||U||_F + eps_ns)
   int64_t rp, cp;
@@ -60,9 +63,12 @@ struct NsParams {
   float a, b, c;    // quintic coefficients
   float lr, decay;
   float dscale;     // 1, or gamma for the scalar-controlled ablation
-  int32_t iter;     // 0 .. 4
-  int32_t last;     // iter == NS iterations - 1
+  int32_t src;      // iterate read by the Gram / apply: 0 XT, 1 XTn (the apply writes the other)
+  int32_t use_alpha;  // the iterate read is the unscaled X0: fold alpha (apply) or alpha^2 (Gram)
+  int32_t last;     // the apply writes the parameters instead of the next iterate
   int32_t write_d;
+  int32_t sx, sy, so; // split matrices: first operand, second operand, output (indices into S / dS)
+  float xshift, yshift; // added to the diagonals of operands sx and sy (P = aI + B is B with shift a)
 };
 
 // Work item of the tiled kernels.
@@ -99,7 +105,7 @@ hipError_t launch_ns_prologue(DType gt, const MatDesc* md, const Item* items, in
                               const NsParams& p, hipStream_t s);
 hipError_t launch_ns_alpha(const MatDesc* md, const int32_t* mats, int32_t nmats,
                            const NsParams& p, hipStream_t s);
-enum GemmKind : int32_t { GEMM_GRAM = 0, GEMM_POLY = 1, GEMM_APPLY = 2 };
+enum GemmKind : int32_t { GEMM_GRAM = 0, GEMM_POLY = 1, GEMM_APPLY = 2, GEMM_SPROD = 3 };
 hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item* items,
                           int32_t nitems, const NsParams& p, hipStream_t s);
 

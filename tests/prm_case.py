@@ -84,14 +84,15 @@ def bf16_write_bound(W_gpu, W_or, D_gpu, D_or, lr) -> float:
     return float(np.max(np.abs(W_gpu - W_or) / bound))
 
 
-def ns_chunks(shapes, budget=32 << 30, tile=256):
+def ns_chunks(shapes, budget=48 << 30, tile=256, plain=False):
     """Which NS5 workspace chunk each matrix lands in, as the library's planner
     packs them (include/prm.h, prm_init): matrices sorted by padded oriented
     shape (r desc, then c desc, ties in list order) are packed in order into
-    chunks of at most `budget` bytes, each matrix taking 4 rp cp + 4 rp^2 +
-    8 rp bytes (regions aligned to 256 bytes).  Returns (chunk index per
-    matrix, largest chunk's bytes); tests check the latter against
-    prm_plan_workspace_bytes."""
+    chunks of at most `budget` bytes, each matrix taking 4 rp cp bytes for its
+    two iterates and 2 rp^2 + 4 rp bytes for each of its split symmetric
+    matrices: four on the factored path (oriented c >= 2r), two otherwise
+    (regions aligned to 256 bytes).  Returns (chunk index per matrix, largest
+    chunk's bytes); tests check the latter against prm_plan_workspace_bytes."""
     def a256(x):
         return (x + 255) // 256 * 256
     rp = [-(-min(m, n) // tile) * tile for m, n in shapes]
@@ -100,7 +101,9 @@ def ns_chunks(shapes, budget=32 << 30, tile=256):
     chunk = [0] * len(shapes)
     k, cur, biggest = -1, 0, 0
     for i in order:
-        need = 2 * a256(rp[i] * cp[i] * 2) + 2 * a256(rp[i] * rp[i] * 2) + 2 * a256(rp[i] * 4)
+        m, n = shapes[i]
+        splits = 4 if (not plain and max(m, n) >= 2 * min(m, n)) else 2
+        need = 2 * a256(rp[i] * cp[i] * 2) + splits * (a256(rp[i] * rp[i] * 2) + a256(rp[i] * 4))
         if k < 0 or cur + need > budget:
             k, cur = k + 1, 0
         chunk[i] = k

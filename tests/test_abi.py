@@ -126,7 +126,7 @@ def test_workspace_fits_dit_configs():
     for wl in synth.WORKLOADS[1:]:
         ws = prm.plan_workspace_bytes(wl.shapes, cfg)
         state = sum(m * n for m, n in wl.shapes) * (2 + 2 + 4)
-        assert ws <= (32 << 30) + (1 << 30)
+        assert ws <= (48 << 30) + (1 << 30)
         assert state + ws < 288e9 * 0.95, wl.name
 
 
@@ -334,4 +334,4 @@ def test_fullsize_sample_covers_every_chunk():
         sample = fs.REFRESH_SAMPLE[wi]
         assert {chunk[i] for i in sample} == set(chunk), wi
         assert {i % 5 for i in sample} == set(range(5)), wi
-    assert len(set(pc.ns_chunks(synth.WORKLOADS[4].shapes)[0])) == 4
+    assert len(set(pc.ns_chunks(synth.WORKLOADS[4].shapes)[0])) == 3

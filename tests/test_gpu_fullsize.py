@@ -6,7 +6,7 @@ The oracle cannot run a whole set, so it checks sampled outputs it can
 compute one by one:
 * refresh step (t = 0): 48 oriented rows of NS5 for every kind of matrix of the
   first and the last block (at DiT-15B: five matrices that cover every kind
-  and each of its four workspace chunks), from the eigendecomposition closed
+  and each of its workspace chunks), from the eigendecomposition closed
   form of the oracle (pinned to the five-iteration map on small inputs):
   relative Frobenius error <= 2e-2 over the sampled rows, and the same bound
   on the worst single sampled row (one wrong row among thousands would hardly
@@ -40,7 +40,7 @@ NO_COPY = (4,)               # too large for a second copy of W and M
 # matrix index = 5 block + kind, kinds qkv, out, mlp up, mlp down, adaLN.
 # Refresh samples: both end blocks x every kind; at DiT-15B (closed form about
 # 15 s per matrix) qkv, out, mlp up and adaLN of block 0 and the last block's
-# mlp down, which lie in its workspace chunks 2, 3, 1, 0 and 2
+# mlp down, which lie in its workspace chunks 1, 2, 0, 0 and 1
 # (test_fullsize_sample_covers_every_chunk checks this on the CPU)
 REFRESH_SAMPLE = {wi: tuple(range(5)) + tuple(range(5 * (synth.WORKLOADS[wi].blocks - 1),
                                                      5 * synth.WORKLOADS[wi].blocks)) for wi in (1, 2, 3)}

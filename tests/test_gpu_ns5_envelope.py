@@ -40,10 +40,12 @@ def envelope(smin):
     return min(0.5, max(2e-2, 1e-4 / max(smin, 1e-300)))
 
 
+@pytest.mark.parametrize("plain", [0, 1])
 @pytest.mark.parametrize("k", [8, 32])
 @pytest.mark.parametrize("noise", [1e-2, 1e-4, 1e-5, 0.0])
-def test_bf16_ns5_envelope(k, noise):
-    cfg = prm.config_default(K=1, lr=0.01, wd=0.0, param_dtype=prm.F32, grad_dtype=prm.F32)
+def test_bf16_ns5_envelope(k, noise, plain):
+    # the wide and tall shapes (c = 3r) run the factored form unless ns_plain
+    cfg = prm.config_default(K=1, lr=0.01, wd=0.0, param_dtype=prm.F32, grad_dtype=prm.F32, ns_plain=plain)
     oc = pc.oracle_config(cfg)
     inputs = [synth.host_matrix(97, i, m, n, k, param_dtype="f32", grad_dtype="f32", noise=noise)
               for i, (m, n) in enumerate(SHAPES)]
@@ -51,7 +53,7 @@ def test_bf16_ns5_envelope(k, noise):
     M = [pc.to_device(m0, 0) for _, m0, _ in inputs]
     G = [pc.to_device(g[0], 0) for _, _, g in inputs]
     D = [torch.zeros(s, dtype=torch.float32, device="cuda") for s in SHAPES]
-    print(f"[envelope] rank {k}, noise {noise:g}", flush=True)
+    print(f"[envelope] rank {k}, noise {noise:g}, {'plain' if plain else 'factored'}", flush=True)
     with prm.Optimizer(SHAPES, cfg) as opt:
         assert opt.step(W, G, M, 0, directions=D) == 1
         torch.cuda.synchronize()

@@ -68,9 +68,9 @@ def check(res, rho, cfg, shapes, lr):
 
 
 @pytest.mark.parametrize("t", [0, 1])
-@pytest.mark.parametrize("wdt,gdt", [(1, 1), (0, 0), (1, 0), (0, 1)])
-def test_ragged_shapes_all_paths(t, wdt, gdt):
-    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=wdt, grad_dtype=gdt)
+@pytest.mark.parametrize("wdt,gdt,plain", [(1, 1, 0), (0, 0, 0), (1, 0, 0), (0, 1, 0), (1, 1, 1)])
+def test_ragged_shapes_all_paths(t, wdt, gdt, plain):
+    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=wdt, grad_dtype=gdt, ns_plain=plain)
     rho, res = run_one_step(RAGGED, cfg, t)
     assert rho == (1 if t == 0 else 0)
     check(res, rho, cfg, RAGGED, cfg.lr)
@@ -82,21 +82,23 @@ def test_ragged_shapes_all_paths(t, wdt, gdt):
 MULTI_TILE = [(700, 2000), (1536, 520), (600, 600), (1300, 1800)]
 
 
-@pytest.mark.parametrize("t,wdt,gdt", [(0, 1, 1), (0, 0, 0), (1, 1, 1)])
-def test_multi_tile_symmetric_products(t, wdt, gdt):
-    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=wdt, grad_dtype=gdt)
+@pytest.mark.parametrize("t,wdt,gdt,plain", [(0, 1, 1, 0), (0, 0, 0, 0), (1, 1, 1, 0), (0, 1, 1, 1), (0, 0, 0, 1)])
+def test_multi_tile_symmetric_products(t, wdt, gdt, plain):
+    # 700 x 2000 and 1536 x 520 (c >= 2r) run NS5 in the factored form unless
+    # ns_plain; 600 x 600 and 1300 x 1800 always run the five iterations
+    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=wdt, grad_dtype=gdt, ns_plain=plain)
     rho, res = run_one_step(MULTI_TILE, cfg, t, workload_id=93)
     assert rho == (1 if t == 0 else 0)
     check(res, rho, cfg, MULTI_TILE, cfg.lr)
 
 
-@pytest.mark.parametrize("flag", ["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh"])
+@pytest.mark.parametrize("flag", ["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh", "ns_plain"])
 @pytest.mark.parametrize("t", [0, 3])
 def test_variants(flag, t):
     shapes = [(96, 320), (300, 88), (64, 64), (33, 130)]
     cfg = prm.config_default(K=3, lr=0.01, wd=0.05, param_dtype=0, grad_dtype=1, **{flag: 1})
     rho, res = run_one_step(shapes, cfg, t, workload_id=91)
-    assert rho == (0 if flag == "never_refresh" else 1)
+    assert rho == (0 if flag == "never_refresh" else (1 if t % 3 == 0 else 0))
     check(res, rho, cfg, shapes, cfg.lr)
 
 
