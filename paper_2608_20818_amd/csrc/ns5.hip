@@ -677,7 +677,78 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     }
   };
   uint16_t* const out = (KIND == GEMM_APPLY) ? XTo : d.S[p.so];
-  if (!last || d.tall) {
+  // Last apply, bf16 W, the tile wholly inside W and W rows a multiple of 8
+  // long: each thread loads the W values of 16 of its 32 chunks before it
+  // writes any of them.  (The compiler cannot tell the W loads from the W
+  // stores apart, so in the loops below each load waits behind the previous
+  // chunk's store, and the epilogue pays the HBM latency chunk after chunk.)
+  bool fastw = false;
+  if constexpr (KIND == GEMM_APPLY && WD == BF16) {
+    fastw = last && (d.n & 7) == 0 &&
+            (d.tall ? (row0 + BM <= d.m && col0 + BN <= d.n) : (col0 + BN <= d.m && row0 + BM <= d.n));
+  }
+  if (fastw) {
+    const float dc = d.s * p.dscale;
+    const int64_t n = d.n;
+    uint16_t* const W = reinterpret_cast<uint16_t*>(d.W);
+    float* const Dm = (p.write_d && d.D) ? d.D : nullptr;
+    // W[wr][wc .. wc + 7] <- decay W - lr dc x, from its loaded value `raw`
+    auto upd = [&](int64_t wr, int64_t wc, const u32x4& raw, const u32x4& xv) __attribute__((always_inline)) {
+      float dv[8], w8[8];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        dv[2 * q] = dc * bf2f(xv[q] & 0xffffu);
+        dv[2 * q + 1] = dc * bf2f(xv[q] >> 16);
+        w8[2 * q] = bf2f(raw[q] & 0xffffu) * p.decay - p.lr * dv[2 * q];
+        w8[2 * q + 1] = bf2f(raw[q] >> 16) * p.decay - p.lr * dv[2 * q + 1];
+      }
+      Vec<uint16_t>::store8(W + wr * n + wc, w8);
+      if (Dm) Vec<float>::store8(Dm + wr * n + wc, dv);
+    };
+    constexpr int NB = 16;
+    if (d.tall) {
+      // the tile of X^T is a tile of W: chunk itr is row 8 itr + tid / 32, columns 8 (tid % 32) ..
+      const int ch = tid & 31;
+#pragma unroll
+      for (int b0 = 0; b0 < BM / 8; b0 += NB) {
+        u32x4 raw[NB];
+#pragma unroll
+        for (int k = 0; k < NB; ++k)
+          raw[k] = *gptr(reinterpret_cast<const u32x4*>(W + (row0 + 8 * (b0 + k) + (tid >> 5)) * n + col0 + ch * 8));
+#pragma unroll
+        for (int k = 0; k < NB; ++k) {
+          const int row = 8 * (b0 + k) + (tid >> 5);
+          upd(row0 + row, col0 + ch * 8, raw[k], *reinterpret_cast<const u32x4*>(tbyte(row, ch * 8)));
+        }
+      }
+    } else {
+      // the mirror of the X^T tile is a tile of W (same lane mapping as below)
+      const int g = lane >> 4, li = lane & 15;
+      constexpr int CB = BN / 16 / NWAVES;
+      static_assert(CB * (BM / 32) == 2 * NB, "two batches of chunks per lane");
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        u32x4 raw[NB];
+#pragma unroll
+        for (int k = 0; k < NB; ++k) {
+          const int cb = half * (CB / 2) + k / (BM / 32), rb = k % (BM / 32);
+          const int C0 = (wave * CB + cb) * 16, R0 = 32 * rb + 8 * g;
+          raw[k] = *gptr(reinterpret_cast<const u32x4*>(W + (col0 + C0 + li) * n + row0 + R0));
+        }
+#pragma unroll
+        for (int k = 0; k < NB; ++k) {
+          const int cb = half * (CB / 2) + k / (BM / 32), rb = k % (BM / 32);
+          const int C0 = (wave * CB + cb) * 16, R0 = 32 * rb + 8 * g;
+          const int sr = R0 + (li >> 2), sc = C0 + 4 * (li & 3);
+          const v4i16 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr, sc));
+          const v4i16 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)tbyte(sr + 4, sc));
+          upd(col0 + C0 + li, row0 + R0, raw[k],
+              __builtin_bit_cast(u32x4, __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7)));
+        }
+      }
+    }
+  }
+  if (!fastw && (!last || d.tall)) {
     const int ch = tid & 31;
     constexpr int ROWS_PER_IT = NTHREADS / 32;
 #pragma unroll 4
@@ -688,7 +759,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
       else wupdate(row0 + row, col0 + ch * 8, w);  // tall: the tile of X^T is a tile of W
     }
   }
-  if ((KIND != GEMM_APPLY && !diag) || (last && !d.tall)) {
+  if (!fastw && ((KIND != GEMM_APPLY && !diag) || (last && !d.tall))) {
     // 16-lane group g reads tile rows R0 .. R0 + 7 (R0 = 32 rb + 8 g) of
     // columns C0 .. C0 + 15; source lane 4 a + b of the group points at
     // row R0 + a (+4), columns C0 + 4 b .. +3
