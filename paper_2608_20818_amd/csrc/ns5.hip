@@ -336,11 +336,18 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // (hi + lo carries 16 mantissa bits; each product is exact in fp32).  Lane L
   // supplies the diagonal entry of column 32 j + L % 32 at element
   // e = L % 32 - 16 h - 8 (L / 32) of k-step half h, when 0 <= e < 8.
-  uint32_t fold_hi[NI], fold_lo[NI];
-  if constexpr (KIND == GEMM_APPLY) {
+  // Split product: the term diag(dX + xshift) Yo is folded the same way on
+  // the other side, as a synthetic first-operand fragment (row 32 i + L % 32
+  // of the wave's rows, same element rule) against the stage's Yo fragments,
+  // while the stage that holds the tile's own rows as k passes through LDS
+  // (Yo is symmetric, so its rows there are the needed columns).
+  static_assert(MI == NI, "one fold array serves row and column blocks");
+  uint32_t fold_hi[MI], fold_lo[MI];
+  if constexpr (KIND == GEMM_APPLY || KIND == GEMM_SPROD) {
 #pragma unroll
-    for (int j = 0; j < NI; ++j) {
-      const float v = p.yshift + d.dS[p.sy][col0 + wn * WN + 32 * j + (lane & 31)];
+    for (int j = 0; j < MI; ++j) {
+      const float v = (KIND == GEMM_APPLY) ? p.yshift + d.dS[p.sy][col0 + wn * WN + 32 * j + (lane & 31)]
+                                           : p.xshift + d.dS[p.sx][row0 + wm * WM + 32 * j + (lane & 31)];
       fold_hi[j] = f2bf(v);
       fold_lo[j] = f2bf(v - bf2f(fold_hi[j]));
     }
@@ -452,10 +459,18 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
         uint32_t hb = fold_hi[J], lb = fold_lo[J];
         asm volatile("" : "+v"(hb), "+v"(lb));
         const bf16x8 hi = syn(hb, ks & 1), lo = syn(lb, ks & 1);
+        if constexpr (KIND == GEMM_SPROD) {
+          // J is the wave's row block here
 #pragma unroll
-        for (int i = 0; i < MI; ++i) mfma(fa[cs][i], hi, acc[i][J]);
+          for (int j = 0; j < NI; ++j) mfma(hi, fb[cs][j], acc[J][j]);
 #pragma unroll
-        for (int i = 0; i < MI; ++i) mfma(fa[cs][i], lo, acc[i][J]);
+          for (int j = 0; j < NI; ++j) mfma(lo, fb[cs][j], acc[J][j]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < MI; ++i) mfma(fa[cs][i], hi, acc[i][J]);
+#pragma unroll
+          for (int i = 0; i < MI; ++i) mfma(fa[cs][i], lo, acc[i][J]);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     };
@@ -485,8 +500,10 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     __syncthreads();
   };
   constexpr std::integral_constant<int, 0> nofold{};
-  // apply: the stage(s) that carry this wave's output columns as k
-  const int kfold = (KIND == GEMM_APPLY) ? (int)((col0 + wn * WN) / BK) : nk;
+  // apply: the stages that carry this wave's output columns as k; split
+  // product: the stages that carry its output rows as k
+  const int kfold = (KIND == GEMM_APPLY) ? (int)((col0 + wn * WN) / BK)
+                    : (KIND == GEMM_SPROD) ? (int)((row0 + wm * WM) / BK) : nk;
   int kt = 0;
   if constexpr (KIND == GEMM_APPLY && WN == BK) {
     // one stage: a run-time flag in a single loop (J is static either way)
@@ -496,10 +513,11 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     // two stages (a stage pair): it runs between two plain loops, since one
     // loop body holding both variants spills.  The pairs before the last one
     // always stream a next stage; the last pair (kt = nk - 2) runs on its own.
-    const int kfirst = (KIND == GEMM_APPLY) ? (kfold & ~1) : nk - 2;  // kfold < nk
+    constexpr bool FOLDS = KIND == GEMM_APPLY || KIND == GEMM_SPROD;
+    const int kfirst = FOLDS ? (kfold & ~1) : nk - 2;  // kfold < nk
     for (; kt < kfirst; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
-    if constexpr (KIND == GEMM_APPLY) {
-      static_assert(WN == 2 * BK, "a wave's output columns span one or two stages");
+    if constexpr (FOLDS) {
+      static_assert(WN == 2 * BK && WM == 2 * BK, "a wave's output columns (rows) span two stages");
       stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, true, true, more_rt);
       kt += 2;
       for (; kt < nk - 2; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
@@ -554,8 +572,6 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     const float* dX = d.dS[p.sx];
     const float* dY = (KIND == GEMM_SPROD) ? d.dS[p.sy] : dX;
     const float ys = (KIND == GEMM_SPROD) ? p.yshift : p.xshift;
-    const uint16_t* Yo = d.S[p.sy];
-    const bool same = p.sx == p.sy;  // split product of a matrix with itself: Yo tile = staged Xo tile
     float dcol[NI][4][4];
     if constexpr (SPLIT) {
 #pragma unroll
@@ -599,15 +615,14 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
               for (int e = 0; e < 4; ++e)
                 v[e] = p.c * acc[i][j][4 * q + e] + (p.b + p.c * (drow[ii] + dcol[j][q][e])) * a4[e];
             } else if constexpr (KIND == GEMM_SPROD) {
-              // (dX + Xo)(dY + Yo) = Xo Yo + dX Yo + Xo dY (+ dX dY on the diagonal)
+              // (dX + Xo)(dY + Yo) = Xo Yo + dX Yo + Xo dY (+ dX dY on the
+              // diagonal); Xo Yo and dX Yo are in acc (the second folded into
+              // the MFMAs), Xo dY comes from the staged Xo tile
               const int ch0 = (wn * WN + 32 * j + 8 * q) >> 3;
               const uint2 w2 = *reinterpret_cast<const uint2*>(trow + ((ch0 ^ (r & 31)) << 4));
               const float a4[4] = {bf2f(w2.x & 0xffffu), bf2f(w2.x >> 16), bf2f(w2.y & 0xffffu), bf2f(w2.y >> 16)};
-              float y4[4] = {a4[0], a4[1], a4[2], a4[3]};
-              if (!same) Vec<uint16_t>::load4(Yo + (grow + 32 * i) * rp + gcol + 32 * j + 8 * q, y4);
 #pragma unroll
-              for (int e = 0; e < 4; ++e)
-                v[e] = acc[i][j][4 * q + e] + drow[ii] * y4[e] + a4[e] * dcol[j][q][e];
+              for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e] + a4[e] * dcol[j][q][e];
             } else {
               // X'^T = alpha (XT diag(a + dB) + XT Bo); both terms are in acc
 #pragma unroll
