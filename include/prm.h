@@ -287,7 +287,9 @@ int prm_peak_hbm(void* hip_stream, uint64_t bytes, double* read_gbs, double* wri
  * steps) live in one static device array of PRM_NOALLOC_SCRATCH_BYTES per GPU,
  * which the library holds on every GPU it runs on until the process ends.  A
  * step that needs more is refused with PRM_ENOMEM before anything is enqueued
- * (refresh steps fit matrices up to about 3072 x 18432; row-wise steps of wide
+ * (a refresh step needs 4 rp cp + 8 rp^2 bytes in the factored form, c >= 2r,
+ * and 4 rp cp + 4 rp^2 otherwise, with rp x cp the oriented shape padded to
+ * 256: 3072 x 12288 and 5120 x 5120 fit, 3072 x 18432 does not; row-wise steps of wide
  * matrices need no workspace).  Every call on one GPU uses the same array:
  * calls that overlap in time on one GPU (on other streams or threads) RACE
  * and give wrong results; calls ordered on one stream are safe, and every byte
