@@ -275,7 +275,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}, WORLD_SIZE "
+        print(f"bench.py: the optimizer runs on one GPU only (got --gpus {args.gpus}, WORLD_SIZE "
               f"{world}); the multi-GPU sharding is a design note, not an implemented path.",
               file=sys.stderr, flush=True)
         sys.exit(2)
