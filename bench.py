@@ -16,6 +16,9 @@ After the timed window one more period runs with per-kernel HIP events
 algorithmic FLOPs (or bytes) per launch over its mean launch time give the
 ``roofline`` object.  The oracle (fp64 NumPy) is timed on a bounded sample of
 the same workload on the host cores and extrapolated (``cpu_baseline``).
+Unless ``--no-other-workloads`` is given, the other DiT-shaped weight sets are
+then timed the same way, one after the other (``other_workloads``: refresh,
+row-wise and amortized times with their fractions of the spec).
 
 Only rank 0 at N = 1 runs; there is no multi-GPU path.
 """
@@ -56,6 +59,8 @@ def parse():
     ap.add_argument("--grad-dtype", choices=["bf16", "f32"], default=None,
                     help="gradient storage dtype (default: the workload's, bf16 for the DiT-shaped sets)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip timing the other DiT weight sets after the headline one")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel attribution period")
     ap.add_argument("--no-aux", action="store_true", help="skip timing the aux-group AdamW step")
     ap.add_argument("--no-peaks", action="store_true",
@@ -135,6 +140,58 @@ def make_inputs(wl_idx, wl, device):
             log(f"[bench] inputs {i + 1}/{len(wl.shapes)} ({time.time() - t0:.1f}s)")
     torch.cuda.synchronize()
     return W, M, G
+
+
+def other_workload(wl_idx, dev, stream):
+    """Refresh and row-wise step times of another weight set (its own K): K
+    warmup steps, then 2K timed steps, each bracketed by HIP events on the
+    optimizer's stream.  Frees its tensors before returning."""
+    import torch
+
+    import paper_2608_20818_amd as prm
+    import synth
+    from oracle import prm_oracle as po
+
+    wl = synth.WORKLOADS[wl_idx]
+    shapes = list(wl.shapes)
+    dt = {"f32": prm.F32, "bf16": prm.BF16}
+    K = wl.K
+    cfg = prm.config_default(K=K, lr=wl.lr, wd=wl.wd, gamma=wl.gamma, beta=wl.beta,
+                             param_dtype=dt[wl.param_dtype], grad_dtype=dt[wl.grad_dtype])
+    log(f"[bench] other workload {wl.name}: {len(shapes)} matrices, K={K}")
+    W, M, G = make_inputs(wl_idx, wl, dev)
+    per, kinds = [], []
+    with prm.Optimizer(shapes, cfg, stream=stream.cuda_stream) as opt:
+        t = 0
+        for _ in range(K):
+            opt.step(W, G, M, t)
+            t += 1
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(2 * K)]
+        for e0, e1 in evs:
+            e0.record(stream)
+            kinds.append(opt.step(W, G, M, t))
+            e1.record(stream)
+            t += 1
+        torch.cuda.synchronize()
+        per = [a.elapsed_time(b) for a, b in evs]
+    del W, M, G
+    torch.cuda.empty_cache()
+    T_ref = statistics.median([x for x, k in zip(per, kinds) if k == 1])
+    T_rw = statistics.median([x for x, k in zip(per, kinds) if k == 0])
+    wb = 2 if wl.param_dtype == "bf16" else 4
+    gb = 2 if wl.grad_dtype == "bf16" else 4
+    elems = sum(m * n for m, n in shapes)
+    ns_flops = sum(po.ns5_flops(m, n) for m, n in shapes)
+    rw_bytes = elems * (gb + 4 + 4 + 2 * wb)
+    log(f"[bench] {wl.name}: refresh {T_ref:.2f} ms, row-wise {T_rw:.3f} ms")
+    return {"workload": wl.name, "matrices": len(shapes), "elements": elems, "K": K,
+            "refresh_ms": T_ref, "rowwise_ms": T_rw,
+            "amortized_ms": (T_ref + (K - 1) * T_rw) / K,
+            "amortized_ms_by_K": {str(k): (T_ref + (k - 1) * T_rw) / k for k in (1, 3, 5, 10)},
+            "single_gpu_reduction_K3_vs_K1": (T_ref - (T_ref + 2 * T_rw) / 3) / T_ref,
+            "refresh_alg_tflops_frac": ns_flops / (T_ref * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+            "rowwise_hbm_frac": rw_bytes / (T_rw * 1e-3) / (PEAK_HBM_GBS * 1e9)}
 
 
 def aux_adamw(wl_idx, wl, dev, stream, steps: int = 50, warmup: int = 5):
@@ -455,10 +512,15 @@ def main():
                 mp = mf["tflops"] if rf["bound"] == "mfma" else mix
                 rf["measured_peak"] = mp
                 rf["frac_of_measured"] = rf["achieved"] / mp
+    del W, M, G
+    torch.cuda.empty_cache()
+    others = None
+    if not args.no_other_workloads and not args.variant and args.grad_dtype is None:
+        # the other DiT-shaped weight sets, one after the other (the headline
+        # set's tensors are freed first: DiT-15B alone holds 181 GB)
+        others = [other_workload(i, dev, stream) for i in range(1, len(synth.WORKLOADS)) if i != args.config]
     cpu = None
     if not args.no_cpu_baseline:
-        del W, M, G
-        torch.cuda.empty_cache()
         log("[bench] timing the oracle on the host (bounded sample)")
         cpu = cpu_baseline(args.config, wl, K, dict(beta=wl.beta, lr=wl.lr, wd=wl.wd, gamma=wl.gamma))
 
@@ -507,6 +569,7 @@ def main():
         "amortized_with_aux_ms": amort + aux["ms"] if aux else None,
         "kernels": kernels,
         "cpu_baseline": cpu,
+        "other_workloads": others,
         "paper_context": "46.9-54.3% optimizer-time reduction of PRM (K=3) vs Muon on 256 H100 with "
                          "FSDP2, normalized units, communication included",
     }
