@@ -7,7 +7,6 @@ paper's printed hyperparameters.  The mutation test plants plausible mistakes
 in the oracle and checks that a pin catches each one.
 """
 import json
-import math
 import os
 
 import numpy as np

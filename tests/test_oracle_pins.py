@@ -14,7 +14,6 @@ import os
 import numpy as np
 import pytest
 
-import oracle
 from oracle import prm_oracle as po
 
 GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_constants.json")))
