@@ -92,6 +92,42 @@ def test_multi_tile_symmetric_products(t, wdt, gdt, plain):
     check(res, rho, cfg, MULTI_TILE, cfg.lr)
 
 
+# the dispatcher's switch between the two exact forms of NS5: oriented
+# c >= 2r runs the factored form (split products between two Grams), c < 2r
+# the five iterations as written; both sides of the boundary, wide and tall
+THRESHOLD = {"factored": [(300, 600), (600, 300), (256, 512)], "plain": [(300, 599), (599, 300), (257, 512)]}
+
+
+@pytest.mark.parametrize("form", ["factored", "plain"])
+@pytest.mark.parametrize("wdt,gdt", [(1, 1), (0, 0)])
+def test_factored_form_threshold(form, wdt, gdt):
+    shapes = THRESHOLD[form]
+    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=wdt, grad_dtype=gdt)
+    inputs = pc.host_inputs(shapes, cfg, 94, steps=(0,))
+    W = [pc.to_device(w, cfg.param_dtype) for w, _, _ in inputs]
+    M = [pc.to_device(m, 0) for _, m, _ in inputs]
+    G = [pc.to_device(g[0], cfg.grad_dtype) for _, _, g in inputs]
+    D = [torch.zeros(sh, dtype=torch.float32, device="cuda") for sh in shapes]
+    with prm.Optimizer(shapes, cfg) as opt:
+        opt.profile_enable(True)
+        assert opt.step(W, G, M, 0, directions=D) == 1
+        torch.cuda.synchronize()
+        stats = opt.profile_read()
+    # the split product runs only in the factored form; the plain form runs
+    # one Gram, one square and one apply launch per iteration
+    if form == "factored":
+        assert stats["ns_sprod"]["launches"] == 9 and stats["ns_gram"]["launches"] == 2, stats
+    else:
+        assert stats["ns_sprod"]["launches"] == 0 and stats["ns_gram"]["launches"] == 5, stats
+    oc = pc.oracle_config(cfg)
+    res = []
+    for i, (w0, m0, g) in enumerate(inputs):
+        Wo, Mo, Do, rho_o = po.step_matrix(w0, m0, g[0], 0, oc)
+        assert rho_o == 1
+        res.append(dict(W=pc.to_host(W[i]), M=pc.to_host(M[i]), D=pc.to_host(D[i]), Wo=Wo, Mo=Mo, Do=Do, W0=w0))
+    check(res, 1, cfg, shapes, cfg.lr)
+
+
 @pytest.mark.parametrize("flag", ["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh", "ns_plain"])
 @pytest.mark.parametrize("t", [0, 3])
 def test_variants(flag, t):
