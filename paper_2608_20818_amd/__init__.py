@@ -386,3 +386,11 @@ class AuxAdamW:
             self.close()
         except Exception:
             pass
+
+
+def __getattr__(name):
+    # the torch.optim adapter imports torch; load it on first use
+    if name == "PRMOptimizer":
+        from .torch_optim import PRMOptimizer
+        return PRMOptimizer
+    raise AttributeError(f"module {__name__!r} has no attribute {name!r}")
