@@ -53,7 +53,8 @@ def parse():
                     help="workload index: 0 tiny, 1 DiT-1.3B, 2 DiT-4B (default), 3 DiT-9B, 4 DiT-15B")
     ap.add_argument("--K", type=int, default=None, help="refresh period (default: the workload's)")
     ap.add_argument("--variant", action="append", default=[],
-                    choices=["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh", "ns_plain"],
+                    choices=["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh", "ns_plain",
+                             "ns_precise"],
                     help="ablation flags of the configuration (repeatable); the default is the paper's method")
     ap.add_argument("--grad-dtype", choices=["bf16", "f32"], default=None,
                     help="gradient storage dtype (default: the workload's, bf16 for the DiT-shaped sets)")

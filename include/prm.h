@@ -90,6 +90,15 @@ typedef struct prm_config {
   int32_t ns_plain;      /* 0 (default): matrices with c >= 2r (oriented) evaluate NS5
                             through the factored form described at prm_step; 1: the
                             five iterations as written for every matrix */
+  int32_t ns_precise;    /* 0 (default); 1: the five iterations as written, with every
+                            iterate carried as two bf16 parts (hi + lo, 16 mantissa bits):
+                            the Gram sums X_hi X_hi^T + X_hi X_lo^T + X_lo X_hi^T and the
+                            apply takes both parts.  It follows the exact NS5 map within
+                            2e-2 also for momenta of low numerical rank, which the bf16
+                            iterate amplifies in its smallest directions,
+                            at 3.3x the default's refresh time at DiT-4B (2.2x the plain
+                            path's) and twice the iterate workspace.  Not available in
+                            prm_step_noalloc. */
   uint64_t workspace_budget_bytes; /* NS5 workspace cap; 0 = automatic (48 GiB) */
 } prm_config;
 
@@ -119,7 +128,7 @@ int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* 
  * NS5 refresh or gamma RowNorm, shape scale, decoupled weight decay and the
  * parameter write), enqueued on the context's stream.
  * NS5 (eq. app-ns-recurrence) is evaluated in one of two exact forms.  For a
- * matrix whose oriented shape has c >= 2r (unless cfg.ns_plain): every B_j
+ * matrix whose oriented shape has c >= 2r (unless cfg.ns_plain or cfg.ns_precise): every B_j
  * is a polynomial in A_0, so the factors P_j = aI + B_j commute, and the
  * step computes X_2 = (P_1 P_0) X_0, A_1 = P_0^2 A_0, A_3 = P_2^2 A_2,
  * A_4 = P_3^2 A_3 and X_5 = (P_4 P_3 P_2) X_2 with r x r products, forming

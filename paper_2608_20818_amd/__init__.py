@@ -43,7 +43,7 @@ class Config(ctypes.Structure):
         ("ns_c", ctypes.c_float), ("nesterov", ctypes.c_int32), ("ema_dampening", ctypes.c_int32),
         ("scale_mode", ctypes.c_int32), ("param_dtype", ctypes.c_int32),
         ("grad_dtype", ctypes.c_int32), ("never_refresh", ctypes.c_int32),
-        ("gamma_on_refresh", ctypes.c_int32), ("ns_plain", ctypes.c_int32),
+        ("gamma_on_refresh", ctypes.c_int32), ("ns_plain", ctypes.c_int32), ("ns_precise", ctypes.c_int32),
         ("workspace_budget_bytes", ctypes.c_uint64),
     ]
 

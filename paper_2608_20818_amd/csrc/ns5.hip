@@ -36,6 +36,10 @@
 // between two explicit iterates (every B_j is a polynomial in A_0, so the
 // factors aI + B_j commute: X_2 = P_1 P_0 X_0, A_{j+1} = P_j^2 A_j,
 // X_5 = P_4 P_3 P_2 X_2).
+// In precise mode the plain iterations carry the iterate as two bf16 parts
+// (hi + lo): the prologue writes both, the Gram sums three products and the
+// apply two over K segments of one accumulation, and the apply writes the next
+// iterate as hi + lo.
 // The workspace is padded to whole tiles and the padding stays exactly zero
 // through every iteration, so the GEMMs need no bounds checks.
 #include <type_traits>
@@ -54,13 +58,15 @@ template <> struct NsStore<BF16> { using T = uint16_t; };
 // ---------------------------------------------------------------------------
 // prologue
 // ---------------------------------------------------------------------------
-template <DType GD>
+// HILO (precise mode): the low bf16 part u - bf16(u) goes to XTl as well.
+template <DType GD, bool HILO>
 __global__ __launch_bounds__(256) void ns_prologue_kernel(const MatDesc* __restrict__ md,
                                                           const Item* __restrict__ items,
                                                           NsParams p) {
   using GT = typename NsStore<GD>::T;
   constexpr int T = kPrologueTile;  // 64
   __shared__ uint16_t tile[T][T + 4];
+  __shared__ uint16_t tile_lo[HILO ? T : 1][T + 4];
   __shared__ float red[4];
   const Item it = items[blockIdx.x];
   const MatDesc& d = md[it.mat];
@@ -107,13 +113,27 @@ __global__ __launch_bounds__(256) void ns_prologue_kernel(const MatDesc* __restr
 #pragma unroll
     for (int k = 0; k < 4; ++k) ss += u[k] * u[k];
     const uint32_t h0 = f2bf(u[0]), h1 = f2bf(u[1]), h2 = f2bf(u[2]), h3 = f2bf(u[3]);
+    uint32_t l0 = 0, l1 = 0, l2 = 0, l3 = 0;
+    if constexpr (HILO) {
+      l0 = f2bf(u[0] - bf2f(h0));
+      l1 = f2bf(u[1] - bf2f(h1));
+      l2 = f2bf(u[2] - bf2f(h2));
+      l3 = f2bf(u[3] - bf2f(h3));
+    }
     if (tall) {
       *reinterpret_cast<uint2*>(XT + row * ld + col) = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
+      if constexpr (HILO) *reinterpret_cast<uint2*>(d.XTl + row * ld + col) = make_uint2(l0 | (l1 << 16), l2 | (l3 << 16));
     } else {
       tile[r][tc + 0] = (uint16_t)h0;
       tile[r][tc + 1] = (uint16_t)h1;
       tile[r][tc + 2] = (uint16_t)h2;
       tile[r][tc + 3] = (uint16_t)h3;
+      if constexpr (HILO) {
+        tile_lo[r][tc + 0] = (uint16_t)l0;
+        tile_lo[r][tc + 1] = (uint16_t)l1;
+        tile_lo[r][tc + 2] = (uint16_t)l2;
+        tile_lo[r][tc + 3] = (uint16_t)l3;
+      }
     }
   }
   if (!tall) {  // uniform per work group
@@ -125,6 +145,11 @@ __global__ __launch_bounds__(256) void ns_prologue_kernel(const MatDesc* __restr
                      v3 = tile[tc + 3][j];
       *reinterpret_cast<uint2*>(XT + (C0 + j) * ld + R0 + tc) =
           make_uint2(v0 | (v1 << 16), v2 | (v3 << 16));
+      if constexpr (HILO) {
+        const uint32_t w0 = tile_lo[tc + 0][j], w1 = tile_lo[tc + 1][j], w2 = tile_lo[tc + 2][j],
+                       w3 = tile_lo[tc + 3][j];
+        *reinterpret_cast<uint2*>(d.XTl + (C0 + j) * ld + R0 + tc) = make_uint2(w0 | (w1 << 16), w2 | (w3 << 16));
+      }
     }
   }
   ss = block_sum<256>(ss, red);
@@ -207,7 +232,11 @@ typedef __attribute__((address_space(3))) v4i16* lds_v4i16;
 // The operands enter the MFMAs swapped, so each lane accumulates four
 // consecutive output columns of one output row (see the epilogue).  WD is the
 // parameter type, used by the parameter write of the last apply.
-template <int KIND, DType WD>
+// NSEG > 1 (precise mode): K runs over NSEG segments with their own operand
+// panels, so one accumulation sums several products: the Gram (NSEG = 3)
+// X_hi X_hi^T + X_hi X_lo^T + X_lo X_hi^T, the apply (NSEG = 2) the factor
+// applied to X_hi and to X_lo, whose result it then writes as hi + lo.
+template <int KIND, DType WD, int NSEG>
 __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDesc* __restrict__ md,
                                                          const Item* __restrict__ items,
                                                          NsParams p) {
@@ -222,7 +251,10 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const uint16_t* XTc = p.src == 0 ? d.XT : d.XTn;
   uint16_t* XTo = p.src == 0 ? d.XTn : d.XT;
+  const uint16_t* XTcl = p.src == 0 ? d.XTl : d.XTnl;   // precise mode: low parts
+  uint16_t* XTol = p.src == 0 ? d.XTnl : d.XTl;
   const int64_t rp = d.rp, cp = d.cp;
+  static_assert(NSEG == 1 || (KIND == GEMM_GRAM && NSEG == 3) || (KIND == GEMM_APPLY && NSEG == 2), "segments");
 
   // C[row][col] = sum_k P[row][k] Q[col][k]   (NT), or
   // C[row][col] = sum_k P[k][row] Q[k][col]   (TN, the Gram on XT)
@@ -241,6 +273,18 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   }
   const int64_t row0 = (int64_t)it.tm * BM, col0 = (int64_t)it.tn * BN;
   const int nk = (int)(klen / BK);  // a multiple of 4: the padded dimensions are multiples of the tile
+  const int NK = NSEG * nk;         // stages over all segments
+  // operand panels of each segment (segment 0: P, Q)
+  const uint16_t* Ps[NSEG];
+  const uint16_t* Qs[NSEG];
+  Ps[0] = P;
+  Qs[0] = Q;
+  if constexpr (KIND == GEMM_GRAM && NSEG == 3) {
+    Ps[1] = XTc; Qs[1] = XTcl;
+    Ps[2] = XTcl; Qs[2] = XTc;
+  } else if constexpr (KIND == GEMM_APPLY && NSEG == 2) {
+    Ps[1] = XTcl; Qs[1] = Q;
+  }
 
   // DMA sources.  NT: wave load q covers tile rows R wave + 8 q + lane / 8
   // (R = ROWS_PER_WAVE, a multiple of 16) and lane fills physical chunk lane % 8,
@@ -253,19 +297,25 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // offset fixed for the whole tile (the row or k-row, and the swizzled chunk),
   // so issuing a load takes no 64-bit vector address arithmetic.  The offsets
   // stay below 2^31 (at most 64 rows of 2^24 bf16).
-  const char *baseA, *baseB;
+  const char *baseA[NSEG], *baseB[NSEG];
   uint32_t voff[DMA_PER_WAVE];
   if constexpr (TN) {
-    baseA = reinterpret_cast<const char*>(P + (int64_t)(KROWS_PER_WAVE * wave) * ld + row0);
-    baseB = reinterpret_cast<const char*>(Q + (int64_t)(KROWS_PER_WAVE * wave) * ld + col0);
+#pragma unroll
+    for (int sg = 0; sg < NSEG; ++sg) {
+      baseA[sg] = reinterpret_cast<const char*>(Ps[sg] + (int64_t)(KROWS_PER_WAVE * wave) * ld + row0);
+      baseB[sg] = reinterpret_cast<const char*>(Qs[sg] + (int64_t)(KROWS_PER_WAVE * wave) * ld + col0);
+    }
 #pragma unroll
     for (int qq = 0; qq < DMA_PER_WAVE; ++qq) {
       const int krow = 2 * qq + (lane >> 5);  // + KR wave, which is 0 mod 4
       voff[qq] = (uint32_t)((krow * ld + (((lane & 31) ^ swz_tn_f(krow)) << 3)) * 2);
     }
   } else {
-    baseA = reinterpret_cast<const char*>(P + (row0 + ROWS_PER_WAVE * wave) * ld);
-    baseB = reinterpret_cast<const char*>(Q + (col0 + ROWS_PER_WAVE * wave) * ld);
+#pragma unroll
+    for (int sg = 0; sg < NSEG; ++sg) {
+      baseA[sg] = reinterpret_cast<const char*>(Ps[sg] + (row0 + ROWS_PER_WAVE * wave) * ld);
+      baseB[sg] = reinterpret_cast<const char*>(Qs[sg] + (col0 + ROWS_PER_WAVE * wave) * ld);
+    }
     // swz_f(row) = 4 (q % 2) + lane / 16, so the lane's source chunk only
     // depends on the parity of q: chunk bit 2 flips for odd q, i.e.
     // (c ^ 4) * 8 elements = c * 8 +- 32
@@ -286,10 +336,22 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // save around the asm; in these kernels its own code reads M0 only for the
   // square epilogue's LDS DMA and writes it right before each such read (the
   // compiled assembly is checked for this by tests/test_abi.py).
-  auto dma1 = [&](char* stage, int64_t k, int q) __attribute__((always_inline)) {
+  // `sg`: the K segment (0 unless NSEG > 1), `k` the offset within it
+  auto dma1 = [&](char* stage, int sg, int64_t k, int q) __attribute__((always_inline)) {
     const bool isb = q >= DMA_PER_WAVE;
     const int qq = isb ? q - DMA_PER_WAVE : q;
-    const char* base = (isb ? baseB : baseA) + (TN ? k * ld : k) * 2;
+    const char* b0 = isb ? baseB[0] : baseA[0];
+    if constexpr (NSEG >= 2) {
+      if (sg == 1) b0 = isb ? baseB[1] : baseA[1];
+      if constexpr (NSEG >= 3) {
+        if (sg == 2) b0 = isb ? baseB[NSEG - 1] : baseA[NSEG - 1];
+      }
+      // the segment is wave-uniform; say so, so that the base stays scalar
+      const uint64_t u = (uint64_t)(uintptr_t)b0;
+      b0 = (const char*)(uintptr_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(u >> 32)) << 32) |
+                                    (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)u));
+    }
+    const char* base = b0 + (TN ? k * ld : k) * 2;
     const uint32_t lds = (uint32_t)(uintptr_t)(lds_ptr)(stage + (isb ? A_BYTES : 0) + (DMA_PER_WAVE * wave + qq) * 1024);
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"  // the M0 clobber, see above
@@ -399,7 +461,10 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     constexpr int MORE = decltype(morec)::value;
     const char* a = cur;
     const char* b = cur + A_BYTES;
-    const int64_t kn = (int64_t)knext * BK;
+    // segment of stage knext (comparisons, not a division, so that it stays a
+    // wave-uniform scalar for the load addresses)
+    const int sgn = NSEG == 1 ? 0 : (int)(knext >= nk) + (NSEG >= 3 ? (int)(knext >= 2 * nk) : 0);
+    const int64_t kn = (int64_t)(knext - sgn * nk) * BK;
     const bool more = MORE == 1 || (MORE == -1 && knext >= 0);
     // two transposing reads give lane L the column (L % 32) of the block at 8
     // consecutive k: k-rows 16 ks + 8 (L / 32) + 4 kk + s, s = 0..3
@@ -426,7 +491,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     static_assert(PRM_DMA_KSTEPS >= 1 && PRM_DMA_KSTEPS <= 3, "loads must be issued before the last k-step");
     if (more) {
 #pragma unroll
-      for (int q = 0; q < DMA0; ++q) dma1(nxt, kn, q);
+      for (int q = 0; q < DMA0; ++q) dma1(nxt, sgn, kn, q);
     }
 #pragma unroll
     for (int i = 0; i < MI; ++i) rda(0, i, 0);
@@ -443,7 +508,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
           if (ks < PRM_DMA_KSTEPS && more) {
             const int slot = ks * MI + i;
 #pragma unroll
-            for (int q = DMA0 + REM * slot / NS; q < DMA0 + REM * (slot + 1) / NS; ++q) dma1(nxt, kn, q);
+            for (int q = DMA0 + REM * slot / NS; q < DMA0 + REM * (slot + 1) / NS; ++q) dma1(nxt, sgn, kn, q);
           }
           rda(cs ^ 1, i, ks + 1);
           if (i < NI) rdb(cs ^ 1, i, ks + 1);
@@ -483,19 +548,19 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
 
   // stage 0 up front, then ping-pong: s0 holds even stages, s1 odd ones
 #pragma unroll
-  for (int q = 0; q < NDMA; ++q) dma1(s0, 0, q);
+  for (int q = 0; q < NDMA; ++q) dma1(s0, 0, 0, q);
   stage_landed();
   __syncthreads();
   constexpr std::integral_constant<int, 1> more_yes{};
   constexpr std::integral_constant<int, 0> more_no{};
   constexpr std::integral_constant<int, -1> more_rt{};
-  // stages kt (in s0) and kt + 1 (in s1); nk is even, so stage kt + 1 exists,
-  // and m1 says whether stage kt + 2 does
+  // stages kt (in s0) and kt + 1 (in s1), counted over all segments; nk is
+  // even, so stage kt + 1 exists, and m1 says whether stage kt + 2 does
   auto stage_pair = [&](int kt, auto f0, auto f1, bool fold0, bool fold1, auto m1) __attribute__((always_inline)) {
     stage_compute(s0, s1, kt + 1, f0, fold0, more_yes);
     stage_landed();
     __syncthreads();  // stage kt+1 has landed; every wave is done with s0
-    stage_compute(s1, s0, kt + 2 < nk ? kt + 2 : -1, f1, fold1, m1);
+    stage_compute(s1, s0, kt + 2 < NK ? kt + 2 : -1, f1, fold1, m1);
     stage_landed();
     __syncthreads();
   };
@@ -507,22 +572,28 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   int kt = 0;
   if constexpr (KIND == GEMM_APPLY && WN == BK) {
     // one stage: a run-time flag in a single loop (J is static either way)
+    static_assert(NSEG == 1, "one segment with this wave layout");
     constexpr std::integral_constant<int, -1> fold_rt{};
     for (; kt < nk; kt += 2) stage_pair(kt, fold_rt, fold_rt, kt == kfold, kt + 1 == kfold, more_rt);
   } else {
     // two stages (a stage pair): it runs between two plain loops, since one
     // loop body holding both variants spills.  The pairs before the last one
-    // always stream a next stage; the last pair (kt = nk - 2) runs on its own.
+    // always stream a next stage; the last pair (kt = NK - 2) runs on its own.
+    // With several segments the fold pair recurs in each (the diagonal term
+    // applies to every part of the iterate).
     constexpr bool FOLDS = KIND == GEMM_APPLY || KIND == GEMM_SPROD;
-    const int kfirst = FOLDS ? (kfold & ~1) : nk - 2;  // kfold < nk
-    for (; kt < kfirst; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
     if constexpr (FOLDS) {
       static_assert(WN == 2 * BK && WM == 2 * BK, "a wave's output columns (rows) span two stages");
-      stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, true, true, more_rt);
-      kt += 2;
-      for (; kt < nk - 2; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
+#pragma unroll
+      for (int sg = 0; sg < NSEG; ++sg) {
+        const int kf = sg * nk + (kfold & ~1);  // kfold < nk
+        for (; kt < kf; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
+        stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, true, true, more_rt);
+        kt += 2;
+      }
     }
-    if (kt < nk) stage_pair(kt, nofold, nofold, false, false, more_no);
+    for (; kt < NK - 2; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
+    if (kt < NK) stage_pair(kt, nofold, nofold, false, false, more_no);
   }
 
   deferred();
@@ -557,6 +628,54 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   }
   const float alpha = p.use_alpha ? *d.alpha : 1.0f;
   const bool last = (KIND == GEMM_APPLY) && p.last;
+  if constexpr (KIND == GEMM_APPLY && NSEG == 2) {
+    if (!last) {
+      // precise mode: the next iterate as hi + lo.  The tile is staged (same
+      // layout as below) and written out twice, as bf16(v) into XTo and as
+      // bf16(v - bf16(v)) into XTol.
+      const int hl = lane >> 5, m = lane & 31;
+      char* T = wm ? s1 : s0;
+      auto tb = [&](int row, int col) __attribute__((always_inline)) {
+        return (row < 128 ? s0 : s1) + (row & 127) * 512 + ((((col >> 3) ^ (row & 31))) << 4) + (col & 7) * 2;
+      };
+#pragma unroll
+      for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int r = 32 * i + m;
+          char* trow = T + r * 512 + 8 * hl;
+#pragma unroll
+          for (int j = 0; j < NI; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              float v[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                v[e] = alpha * acc[i][j][4 * q + e];
+                if (pass) v[e] -= bf2f(f2bf(v[e]));
+              }
+              const int ch = (wn * WN + 32 * j + 8 * q) >> 3;
+              uint2 w;
+              w.x = pack_bf2(v[0], v[1]);
+              w.y = pack_bf2(v[2], v[3]);
+              *reinterpret_cast<uint2*>(trow + ((ch ^ (r & 31)) << 4)) = w;
+            }
+        }
+        __syncthreads();
+        uint16_t* const dst = pass ? XTol : XTo;
+        const int ch = tid & 31;
+        constexpr int ROWS_PER_IT = NTHREADS / 32;
+#pragma unroll 4
+        for (int itr = 0; itr < BM / ROWS_PER_IT; ++itr) {
+          const int row = itr * ROWS_PER_IT + (tid >> 5);
+          *reinterpret_cast<u32x4*>(dst + (row0 + row) * rp + col0 + ch * 8) =
+              *reinterpret_cast<const u32x4*>(tb(row, ch * 8));
+        }
+        __syncthreads();
+      }
+      return;
+    }
+  }
   {
     const float s2 = alpha * alpha;
     char* T = wm ? s1 : s0;
@@ -803,8 +922,13 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
 hipError_t launch_ns_prologue(DType gt, const MatDesc* md, const Item* items, int32_t nitems,
                               const NsParams& p, hipStream_t s) {
   if (nitems <= 0) return hipSuccess;
-  if (gt == BF16) ns_prologue_kernel<BF16><<<dim3(nitems), dim3(256), 0, s>>>(md, items, p);
-  else ns_prologue_kernel<F32><<<dim3(nitems), dim3(256), 0, s>>>(md, items, p);
+  if (p.hilo) {
+    if (gt == BF16) ns_prologue_kernel<BF16, true><<<dim3(nitems), dim3(256), 0, s>>>(md, items, p);
+    else ns_prologue_kernel<F32, true><<<dim3(nitems), dim3(256), 0, s>>>(md, items, p);
+  } else {
+    if (gt == BF16) ns_prologue_kernel<BF16, false><<<dim3(nitems), dim3(256), 0, s>>>(md, items, p);
+    else ns_prologue_kernel<F32, false><<<dim3(nitems), dim3(256), 0, s>>>(md, items, p);
+  }
   return hipGetLastError();
 }
 
@@ -816,16 +940,24 @@ hipError_t launch_ns_alpha(const MatDesc* md, const int32_t* mats, int32_t nmats
 }
 
 hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item* items,
-                          int32_t nitems, const NsParams& p, hipStream_t s) {
+                          int32_t nitems, const NsParams& p, hipStream_t s, bool hilo) {
   if (nitems <= 0) return hipSuccess;
   dim3 g(nitems), b(gemm::NTHREADS);
   switch (kind) {
-    case GEMM_GRAM: ns_gemm_kernel<GEMM_GRAM, BF16><<<g, b, 0, s>>>(md, items, p); break;
-    case GEMM_POLY: ns_gemm_kernel<GEMM_POLY, BF16><<<g, b, 0, s>>>(md, items, p); break;
-    case GEMM_SPROD: ns_gemm_kernel<GEMM_SPROD, BF16><<<g, b, 0, s>>>(md, items, p); break;
+    case GEMM_GRAM:
+      if (hilo) ns_gemm_kernel<GEMM_GRAM, BF16, 3><<<g, b, 0, s>>>(md, items, p);
+      else ns_gemm_kernel<GEMM_GRAM, BF16, 1><<<g, b, 0, s>>>(md, items, p);
+      break;
+    case GEMM_POLY: ns_gemm_kernel<GEMM_POLY, BF16, 1><<<g, b, 0, s>>>(md, items, p); break;
+    case GEMM_SPROD: ns_gemm_kernel<GEMM_SPROD, BF16, 1><<<g, b, 0, s>>>(md, items, p); break;
     case GEMM_APPLY:
-      if (wt == BF16) ns_gemm_kernel<GEMM_APPLY, BF16><<<g, b, 0, s>>>(md, items, p);
-      else ns_gemm_kernel<GEMM_APPLY, F32><<<g, b, 0, s>>>(md, items, p);
+      if (hilo) {
+        if (wt == BF16) ns_gemm_kernel<GEMM_APPLY, BF16, 2><<<g, b, 0, s>>>(md, items, p);
+        else ns_gemm_kernel<GEMM_APPLY, F32, 2><<<g, b, 0, s>>>(md, items, p);
+      } else {
+        if (wt == BF16) ns_gemm_kernel<GEMM_APPLY, BF16, 1><<<g, b, 0, s>>>(md, items, p);
+        else ns_gemm_kernel<GEMM_APPLY, F32, 1><<<g, b, 0, s>>>(md, items, p);
+      }
       break;
     default: return hipErrorInvalidValue;
   }

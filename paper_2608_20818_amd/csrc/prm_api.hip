@@ -127,6 +127,7 @@ struct Plan {
   std::vector<int64_t> m, nn, rp, cp;
   std::vector<int32_t> tall;
   std::vector<int32_t> chain;       // NS5 in the factored form (oriented c >= 2r)
+  int32_t precise = 0;              // every iterate carried as hi + lo bf16 (plain path)
   std::vector<float> s;
   std::vector<uint64_t> ws_off;     // offset of the matrix's NS region inside the chunk area
   std::vector<uint64_t> small_off;  // partial sums + alpha
@@ -160,6 +161,7 @@ int validate_cfg(const prm_config* c) {
   if (c->never_refresh != 0 && c->never_refresh != 1) return fail(PRM_EINVAL, "never_refresh must be 0 or 1");
   if (c->gamma_on_refresh != 0 && c->gamma_on_refresh != 1) return fail(PRM_EINVAL, "gamma_on_refresh must be 0 or 1");
   if (c->ns_plain != 0 && c->ns_plain != 1) return fail(PRM_EINVAL, "ns_plain must be 0 or 1");
+  if (c->ns_precise != 0 && c->ns_precise != 1) return fail(PRM_EINVAL, "ns_precise must be 0 or 1");
   if (c->scale_mode < 0 || c->scale_mode > 2) return fail(PRM_EINVAL, "unknown scale_mode %d", c->scale_mode);
   if (c->param_dtype != PRM_F32 && c->param_dtype != PRM_BF16) return fail(PRM_EDTYPE, "unsupported param_dtype %d", c->param_dtype);
   if (c->grad_dtype != PRM_F32 && c->grad_dtype != PRM_BF16) return fail(PRM_EDTYPE, "unsupported grad_dtype %d", c->grad_dtype);
@@ -174,14 +176,16 @@ float shape_scale(int64_t m, int64_t n, int mode) {
   }
 }
 
-// NS5 workspace of one matrix: the transposed iterate and the next one (bf16),
-// and the split symmetric r x r matrices (bf16 off-diagonal part, fp32
-// diagonal): two on the plain path (A, B), four on the factored one.
+// NS5 workspace of one matrix: the transposed iterate and the next one (bf16;
+// in precise mode also their low parts), and the split symmetric r x r
+// matrices (bf16 off-diagonal part, fp32 diagonal): two on the plain path
+// (A, B), four on the factored one.
 int ns_splits(int chain) { return chain ? 4 : 2; }
-uint64_t ns_matrix_bytes(int64_t rp, int64_t cp, int chain) {
+int ns_iterates(int precise) { return precise ? 4 : 2; }
+uint64_t ns_matrix_bytes(int64_t rp, int64_t cp, int chain, int precise) {
   const uint64_t xs = align256((uint64_t)rp * cp * 2), gs = align256((uint64_t)rp * rp * 2),
                  vs = align256((uint64_t)rp * 4);
-  return 2 * xs + (uint64_t)ns_splits(chain) * (gs + vs);
+  return (uint64_t)ns_iterates(precise) * xs + (uint64_t)ns_splits(chain) * (gs + vs);
 }
 
 // Row-wise launch class of a wide row of length n (0 tpr = generic path).
@@ -203,6 +207,7 @@ int make_plan(int32_t n_mats, const int64_t* rows, const int64_t* cols, const pr
   if (n_mats > 0 && (!rows || !cols)) return fail(PRM_EINVAL, "rows/cols is NULL");
   P = Plan();
   P.n = n_mats;
+  P.precise = cfg->ns_precise;
   for (int i = 0; i < n_mats; ++i) {
     const int64_t m = rows[i], n = cols[i];
     if (m < 1 || n < 1 || m > kMaxDim || n > kMaxDim)
@@ -212,8 +217,9 @@ int make_plan(int32_t n_mats, const int64_t* rows, const int64_t* cols, const pr
     P.nn.push_back(n);
     P.tall.push_back(m > n ? 1 : 0);
     // the factored form needs c >= 2r: it saves work only there, and its
-    // rounding stays below the plain path's only away from square shapes
-    P.chain.push_back(!cfg->ns_plain && c >= 2 * r ? 1 : 0);
+    // rounding stays below the plain path's only away from square shapes;
+    // precise mode runs the plain path
+    P.chain.push_back(!cfg->ns_plain && !cfg->ns_precise && c >= 2 * r ? 1 : 0);
     P.rp.push_back(round_up(r, kNsTile));
     P.cp.push_back(round_up(c, kNsTile));
     P.s.push_back(shape_scale(m, n, cfg->scale_mode));
@@ -250,7 +256,7 @@ int make_plan(int32_t n_mats, const int64_t* rows, const int64_t* cols, const pr
   P.ws_off.assign(n_mats, 0);
   uint64_t cur = 0;
   for (int idx : order) {
-    const uint64_t need = ns_matrix_bytes(P.rp[idx], P.cp[idx], P.chain[idx]);
+    const uint64_t need = ns_matrix_bytes(P.rp[idx], P.cp[idx], P.chain[idx], P.precise);
     if (need > budget)
       return fail(PRM_ENOMEM, "matrix %d needs %llu workspace bytes, budget is %llu", idx,
                   (unsigned long long)need, (unsigned long long)budget);
@@ -430,12 +436,15 @@ void fill_descs(const Plan& P, char* chunk_base, char* small_base, char* tall_ba
     const uint64_t xs = align256((uint64_t)d.rp * d.cp * 2), gs = align256((uint64_t)d.rp * d.rp * 2),
                    vs = align256((uint64_t)d.rp * 4);
     char* w = chunk_base + P.ws_off[i];
+    const int nx = ns_iterates(P.precise);
     d.XT = (uint16_t*)w;
     d.XTn = (uint16_t*)(w + xs);
+    d.XTl = P.precise ? (uint16_t*)(w + 2 * xs) : nullptr;
+    d.XTnl = P.precise ? (uint16_t*)(w + 3 * xs) : nullptr;
     const int ns = ns_splits(P.chain[i]);
     for (int k = 0; k < 4; ++k) {
-      d.S[k] = k < ns ? (uint16_t*)(w + 2 * xs + k * gs) : nullptr;
-      d.dS[k] = k < ns ? (float*)(w + 2 * xs + ns * gs + k * vs) : nullptr;
+      d.S[k] = k < ns ? (uint16_t*)(w + nx * xs + k * gs) : nullptr;
+      d.dS[k] = k < ns ? (float*)(w + nx * xs + ns * gs + k * vs) : nullptr;
     }
     d.ptiles_m = (int32_t)((d.tall ? d.cp : d.rp) / kPrologueTile);
     d.ptiles_n = (int32_t)((d.tall ? d.rp : d.cp) / kPrologueTile);
@@ -618,13 +627,15 @@ int refresh_step(prm_ctx* c, float lr, bool debug) {
   p.decay = 1.0f - lr * cf.wd;
   p.dscale = cf.gamma_on_refresh ? cf.gamma : 1.0f;
   p.write_d = debug ? 1 : 0;
+  p.hilo = P.precise;
+  const bool hilo = P.precise != 0;
   const DType wt = (DType)cf.param_dtype, gt = (DType)cf.grad_dtype;
   const double gb = gt == BF16 ? 2 : 4, wb = wt == BF16 ? 2 : 4, db = debug ? 4 : 0;
   const MatDesc* md = c->d_desc;
   const float a = cf.ns_a;
   int rc;
   for (const auto& ch : P.chunks) {
-    rc = timed(c, K_NS_PROLOGUE, ch.elems * (gb + 8 + 2), 0, [&] {  // G, M read; M, bf16 X^T written
+    rc = timed(c, K_NS_PROLOGUE, ch.elems * (gb + 8 + (hilo ? 4 : 2)), 0, [&] {  // G, M read; M, bf16 X^T (hi, lo) written
       return launch_ns_prologue(gt, md, c->d_items + ch.off_prologue, (int32_t)ch.prologue.size(), p, c->stream);
     });
     if (rc) return rc;
@@ -645,8 +656,8 @@ int refresh_step(prm_ctx* c, float lr, bool debug) {
       auto gram = [&](int src, int alpha, int so) {
         p.src = src; p.use_alpha = alpha; p.so = so;
         return timed(c, K_NS_GRAM, 0, G.alg_rc, [&] {
-          return launch_ns_gemm(GEMM_GRAM, wt, md, upper, nu, p, c->stream);
-        }, G.exec_gram);
+          return launch_ns_gemm(GEMM_GRAM, wt, md, upper, nu, p, c->stream, hilo);
+        }, G.exec_gram * (hilo ? 3 : 1));
       };
       auto poly = [&](int sx, int so) {
         p.sx = sx; p.sy = sx; p.so = so; p.xshift = 0.f; p.yshift = 0.f;
@@ -663,8 +674,8 @@ int refresh_step(prm_ctx* c, float lr, bool debug) {
       auto applyk = [&](int src, int alpha, int sy, float ys, int last) {
         p.src = src; p.use_alpha = alpha; p.sy = sy; p.yshift = ys; p.last = last;
         rc = timed(c, K_NS_APPLY, last ? G.elems * (2 * wb + db) : 0, G.alg_rc, [&] {
-          return launch_ns_gemm(GEMM_APPLY, wt, md, apply, na, p, c->stream);
-        }, G.exec_apply);
+          return launch_ns_gemm(GEMM_APPLY, wt, md, apply, na, p, c->stream, hilo);
+        }, G.exec_apply * (hilo ? 2 : 1));
         p.last = 0;
         return rc;
       };
@@ -1238,6 +1249,7 @@ int prm_step_noalloc(const prm_config* cfg, int64_t rows, int64_t cols, void* pa
                      float* momentum, int64_t step, float lr, int32_t* did_refresh, void* hip_stream) {
   if (!cfg) return fail(PRM_EINVAL, "cfg is NULL");
   if (step < 0) return fail(PRM_EINVAL, "step must be >= 0 (got %lld)", (long long)step);
+  if (cfg->ns_precise) return fail(PRM_EINVAL, "ns_precise is not available in the allocation-free step");
   const float eta = lr < 0.f ? cfg->lr : lr;
   if (!std::isfinite(eta)) return fail(PRM_EINVAL, "lr must be finite");
   // the workspace cap is the scratch array, checked below

@@ -25,6 +25,10 @@ struct MatDesc {
   // iterate is kept transposed, XT = X^T (cp x rp, row-major).
   uint16_t* XT;   // cp x rp   iterate
   uint16_t* XTn;  // cp x rp   next iterate
+  // precise mode only (else nullptr): the low bf16 parts of XT and XTn, so
+  // that each iterate is carried as hi + lo (16 mantissa bits)
+  uint16_t* XTl;
+  uint16_t* XTnl;
   // Symmetric r x r matrices in split form: S[k] (rp x rp, bf16) holds the
   // off-diagonal part (diagonal stored as zero), dS[k] (rp, fp32) the
   // diagonal.  The dispatcher assigns them roles (the Gram matrix A, B =
@@ -69,6 +73,7 @@ struct NsParams {
   int32_t write_d;
   int32_t sx, sy, so; // split matrices: first operand, second operand, output (indices into S / dS)
   float xshift, yshift; // added to the diagonals of operands sx and sy (P = aI + B is B with shift a)
+  int32_t hilo;       // precise mode: the prologue also writes the low parts (XTl)
 };
 
 // Work item of the tiled kernels.
@@ -102,12 +107,15 @@ hipError_t launch_rw_tall_apply(int vec, DType wt, DType gt, const MatDesc* md,
 
 // NS5 refresh.
 hipError_t launch_ns_prologue(DType gt, const MatDesc* md, const Item* items, int32_t nitems,
-                              const NsParams& p, hipStream_t s);
+                              const NsParams& p, hipStream_t s);  // p.hilo: also the low parts
 hipError_t launch_ns_alpha(const MatDesc* md, const int32_t* mats, int32_t nmats,
                            const NsParams& p, hipStream_t s);
 enum GemmKind : int32_t { GEMM_GRAM = 0, GEMM_POLY = 1, GEMM_APPLY = 2, GEMM_SPROD = 3 };
+// hilo (Gram and apply only): the iterate is read as hi + lo; the Gram sums
+// hi hi^T + hi lo^T + lo hi^T, the apply takes both parts and, unless it is
+// the last one, writes the next iterate as hi + lo
 hipError_t launch_ns_gemm(GemmKind kind, DType wt, const MatDesc* md, const Item* items,
-                          int32_t nitems, const NsParams& p, hipStream_t s);
+                          int32_t nitems, const NsParams& p, hipStream_t s, bool hilo = false);
 
 // calibration probes (probe.hip)
 hipError_t launch_probe_mfma(int blocks, float* sink, unsigned long long* clk, int iters, hipStream_t s);

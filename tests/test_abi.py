@@ -38,9 +38,10 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_config_struct_layout_matches_header():
-    # prm_config: 10 x 4-byte scalars, 8 int32 flags, then a uint64
-    assert ctypes.sizeof(prm.Config) == 80
-    assert prm.Config.workspace_budget_bytes.offset == 72
+    # prm_config: 10 x 4-byte scalars, 9 int32 flags, padding, then a uint64
+    assert ctypes.sizeof(prm.Config) == 88
+    assert prm.Config.ns_precise.offset == 72
+    assert prm.Config.workspace_budget_bytes.offset == 80
 
 
 def test_config_defaults_are_paper_values():
@@ -137,7 +138,7 @@ def test_workspace_fits_dit_configs():
     ("eps_rownorm", float("inf"), prm.PRM_EINVAL), ("eps_ns", float("nan"), prm.PRM_EINVAL),
     ("eps_ns", 0.0, prm.PRM_EINVAL), ("eps_ns", -1e-7, prm.PRM_EINVAL),
     ("param_dtype", 5, prm.PRM_EDTYPE), ("grad_dtype", -1, prm.PRM_EDTYPE),
-    ("nesterov", 2, prm.PRM_EINVAL),
+    ("nesterov", 2, prm.PRM_EINVAL), ("ns_plain", 2, prm.PRM_EINVAL), ("ns_precise", 2, prm.PRM_EINVAL),
 ])
 def test_init_validates_before_touching_the_device(field, value, code):
     cfg = prm.config_default(**{field: value})
@@ -335,3 +336,29 @@ def test_fullsize_sample_covers_every_chunk():
         assert {chunk[i] for i in sample} == set(chunk), wi
         assert {i % 5 for i in sample} == set(range(5)), wi
     assert len(set(pc.ns_chunks(synth.WORKLOADS[4].shapes)[0])) == 3
+
+
+def test_precise_mode_plans_the_plain_path_with_hi_lo_iterates():
+    """ns_precise: a wide matrix (c >= 2r) takes the plain path (two split
+    matrices instead of four) and its two iterates gain low parts: the plan
+    grows by 2 rp cp bf16 and shrinks by two split matrices."""
+    L = prm.load()
+    rows = (ctypes.c_int64 * 1)(256)
+    cols = (ctypes.c_int64 * 1)(768)
+    sizes = {}
+    for precise in (0, 1):
+        cfg = prm.config_default(ns_precise=precise)
+        out = ctypes.c_uint64()
+        assert L.prm_plan_workspace_bytes(1, rows, cols, ctypes.byref(cfg), ctypes.byref(out)) == prm.PRM_OK
+        sizes[precise] = out.value
+    xs, gs, vs = 256 * 768 * 2, 256 * 256 * 2, 256 * 4
+    assert sizes[1] - sizes[0] == 2 * xs - 2 * (gs + vs)
+
+
+def test_precise_mode_refused_by_the_allocation_free_step():
+    L = prm.load()
+    cfg = prm.config_default(ns_precise=1)
+    rho = ctypes.c_int32(-1)
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: the config is refused first
+    rc = L.prm_step_noalloc(ctypes.byref(cfg), 4, 8, fake, fake, fake, 0, -1.0, ctypes.byref(rho), None)
+    assert rc == prm.PRM_EINVAL and "ns_precise" in L.prm_last_error().decode()

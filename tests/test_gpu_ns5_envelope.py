@@ -14,6 +14,9 @@ the bf16 iterate in those directions by the same factor.  The stated envelope
 where s^_min is the smallest normalized singular value of the oriented
 momentum.  Inputs: the workloads' recipe (rank-k power-law signal plus
 Gaussian noise) with rank 8 or 32 and noise 1e-2 (control), 1e-4, 1e-5 or 0.
+
+The precise mode (prm_config.ns_precise: every iterate as hi + lo bf16) is
+held to the plain 2e-2 bar on the same inputs, exactly low-rank ones included.
 """
 import os
 import sys
@@ -69,3 +72,25 @@ def test_bf16_ns5_envelope(k, noise, plain):
         assert err <= bound, f"{m}x{n}: D err {err:.3e} above the envelope {bound:.3e} (s^_min {smin:.2e})"
         if noise >= 1e-2:
             assert err <= pc.TOL_NS5
+
+
+@pytest.mark.parametrize("k", [8, 32])
+@pytest.mark.parametrize("noise", [1e-2, 1e-4, 1e-5, 0.0])
+def test_precise_ns5_meets_the_bar_on_low_rank_momenta(k, noise):
+    cfg = prm.config_default(K=1, lr=0.01, wd=0.0, param_dtype=prm.F32, grad_dtype=prm.F32, ns_precise=1)
+    oc = pc.oracle_config(cfg)
+    inputs = [synth.host_matrix(97, i, m, n, k, param_dtype="f32", grad_dtype="f32", noise=noise)
+              for i, (m, n) in enumerate(SHAPES)]
+    W = [pc.to_device(w, 0) for w, _, _ in inputs]
+    M = [pc.to_device(m0, 0) for _, m0, _ in inputs]
+    G = [pc.to_device(g[0], 0) for _, _, g in inputs]
+    D = [torch.zeros(s, dtype=torch.float32, device="cuda") for s in SHAPES]
+    print(f"[precise] rank {k}, noise {noise:g}", flush=True)
+    with prm.Optimizer(SHAPES, cfg) as opt:
+        assert opt.step(W, G, M, 0, directions=D) == 1
+        torch.cuda.synchronize()
+    for i, ((m, n), (w0, m0, g)) in enumerate(zip(SHAPES, inputs)):
+        _, Mo, Do, rho = po.step_matrix(w0, m0, g[0], 0, oc)
+        err = pc.rel(pc.to_host(D[i]), Do)
+        print(f"  {m}x{n} rank {k} noise {noise:g}: D err {err:.3e}", flush=True)
+        assert err <= pc.TOL_NS5, f"{m}x{n}: precise D err {err:.3e} > {pc.TOL_NS5}"

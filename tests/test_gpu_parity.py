@@ -92,6 +92,17 @@ def test_multi_tile_symmetric_products(t, wdt, gdt, plain):
     check(res, rho, cfg, MULTI_TILE, cfg.lr)
 
 
+@pytest.mark.parametrize("t,wdt,gdt", [(0, 1, 1), (0, 0, 0), (4, 0, 1)])
+def test_precise_mode_multi_tile(t, wdt, gdt):
+    """ns_precise (hi + lo iterates) over several tiles with padding: the
+    Gram's three K segments, the apply's two with a fold stage pair in each,
+    the hi + lo write of the next iterate, and the parameter write."""
+    cfg = prm.config_default(K=4, lr=0.02, wd=0.1, param_dtype=wdt, grad_dtype=gdt, ns_precise=1)
+    rho, res = run_one_step(MULTI_TILE, cfg, t, workload_id=95)
+    assert rho == 1
+    check(res, rho, cfg, MULTI_TILE, cfg.lr)
+
+
 # the dispatcher's switch between the two exact forms of NS5: oriented
 # c >= 2r runs the factored form (split products between two Grams), c < 2r
 # the five iterations as written; both sides of the boundary, wide and tall
@@ -128,7 +139,8 @@ def test_factored_form_threshold(form, wdt, gdt):
     check(res, 1, cfg, shapes, cfg.lr)
 
 
-@pytest.mark.parametrize("flag", ["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh", "ns_plain"])
+@pytest.mark.parametrize("flag", ["nesterov", "ema_dampening", "gamma_on_refresh", "never_refresh", "ns_plain",
+                                  "ns_precise"])
 @pytest.mark.parametrize("t", [0, 3])
 def test_variants(flag, t):
     shapes = [(96, 320), (300, 88), (64, 64), (33, 130)]
