@@ -150,12 +150,14 @@ def test_variants(flag, t):
     check(res, rho, cfg, shapes, cfg.lr)
 
 
-def test_several_workspace_chunks():
+@pytest.mark.parametrize("precise", [0, 1])
+def test_several_workspace_chunks(precise):
     shapes = [(256, 512), (512, 256), (128, 640), (200, 200), (256, 512)]
     # a budget that holds the largest single matrix but not all of them
-    one = max(prm.plan_workspace_bytes([s], prm.config_default()) for s in shapes)
-    cfg = prm.config_default(K=2, lr=0.01, wd=0.01, workspace_budget_bytes=one)
-    assert prm.plan_workspace_bytes(shapes, cfg) < prm.plan_workspace_bytes(shapes, prm.config_default())
+    base = prm.config_default(ns_precise=precise)
+    one = max(prm.plan_workspace_bytes([s], base) for s in shapes)
+    cfg = prm.config_default(K=2, lr=0.01, wd=0.01, workspace_budget_bytes=one, ns_precise=precise)
+    assert prm.plan_workspace_bytes(shapes, cfg) < prm.plan_workspace_bytes(shapes, base)
     rho, res = run_one_step(shapes, cfg, 0, workload_id=92)
     check(res, rho, cfg, shapes, cfg.lr)
 
