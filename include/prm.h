@@ -139,7 +139,9 @@ int prm_init(prm_ctx** out, int32_t n_mats, const int64_t* rows, const int64_t* 
  * momentum[i]: M (fp32); all device pointers, 16-byte aligned.  lr < 0 uses
  * cfg->lr.  *did_refresh (nullable) receives rho_t, computed on the host.
  * Runs on the device the context was created on; the caller's current device
- * is restored before returning. */
+ * is restored before returning.  A call whose pointer arrays equal the
+ * previous call's enqueues kernels only (no allocation, memset or upload), so
+ * it may be captured into a HIP graph and replayed for the same rho_t. */
 int prm_step(prm_ctx* ctx, void* const* params, const void* const* grads,
              float* const* momentum, int64_t step, float lr, int32_t* did_refresh);
 
