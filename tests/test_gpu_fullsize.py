@@ -4,7 +4,7 @@ launch configuration bench.py times.
 
 The oracle cannot run a whole set, so it checks sampled outputs it can
 compute one by one:
-* refresh step (t = 0): 48 oriented rows of NS5 for every kind of matrix of the
+* refresh step (t = 0; also in precise mode at DiT-1.3B and 4B): 48 oriented rows of NS5 for every kind of matrix of the
   first and the last block (at DiT-15B: five matrices that cover every kind
   and each of its workspace chunks), from the eigendecomposition closed
   form of the oracle (pinned to the five-iteration map on small inputs):
@@ -60,17 +60,17 @@ def make_set(wi, step):
     return W, M, G
 
 
-def config(WL):
+def config(WL, precise=0):
     return prm.config_default(K=WL.K, lr=WL.lr, wd=WL.wd, gamma=WL.gamma, beta=WL.beta,
-                              param_dtype=prm.BF16, grad_dtype=prm.BF16)
+                              param_dtype=prm.BF16, grad_dtype=prm.BF16, ns_precise=precise)
 
 
-def run(wi, step, sample):
+def run(wi, step, sample, precise=0):
     """One step at the given t over the whole set; returns host copies of the
     sampled matrices' inputs and outputs, and (up to DiT-9B) checks the debug
     step against the timed one bitwise."""
     WL = synth.WORKLOADS[wi]
-    cfg = config(WL)
+    cfg = config(WL, precise)
     shapes = list(WL.shapes)
     print(f"[fullsize] {WL.name} t={step}: drawing {len(shapes)} matrices", flush=True)
     W, M, G = make_set(wi, step)
@@ -121,11 +121,14 @@ def check_rows(WL, cfg, i, rows, Do_rows, host_in, out, tol):
     assert slack <= 1.0, f"matrix {i}: W outside the rounding bound ({slack:.3f})"
 
 
-@pytest.mark.parametrize("wi", SETS, ids=[synth.WORKLOADS[i].name for i in SETS])
-def test_refresh_step_sampled_rows(wi):
+@pytest.mark.parametrize("wi,precise", [(wi, 0) for wi in SETS] + [(1, 1), (2, 1)],
+                         ids=[synth.WORKLOADS[i].name for i in SETS] + ["dit-1.3b-precise", "dit-4b-precise"])
+def test_refresh_step_sampled_rows(wi, precise):
+    """The default path on every set; the precise mode (hi + lo iterates, the
+    plain iterations for every matrix) on DiT-1.3B and DiT-4B."""
     WL = synth.WORKLOADS[wi]
-    sample = list(REFRESH_SAMPLE[wi])             # matrices of block 0
-    cfg, host_in, out = run(wi, 0, sample)
+    sample = list(REFRESH_SAMPLE[wi])             # matrices of the first and last block
+    cfg, host_in, out = run(wi, 0, sample, precise)
     oc = pc.oracle_config(cfg)
     rng = np.random.default_rng(7)
     for i in sample:
