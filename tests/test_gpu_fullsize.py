@@ -15,9 +15,17 @@ compute one by one:
   down projection) of every sampled matrix, error <= 1e-5, per row as well;
 * momentum rows <= 1e-6; bf16 W rows within half an ulp plus eta |D - D_oracle|.
 Up to DiT-9B the non-debug prm_step (what bench.py times) must also produce
-bitwise the same W and M as prm_step_debug on the same inputs.  At DiT-15B
-(W, M and G take 180 GB) there is no room for that second copy, and only the
-sampled matrices get a direction output (NULL entries for the others).
+bitwise the same W and M as prm_step_debug on the same inputs, and every
+matrix of the set is checked, not only the sampled ones:
+* row-wise step: every oriented row of D against RowNorm of the same row of
+  the new momentum (fp64 on the GPU: a norm and a division), <= 1e-5 per row;
+* refresh step: D against the five-iteration map evaluated in fp64 on the GPU
+  (torch matrix products) from the step's new momentum, <= 2e-2 per matrix and
+  per row.  That fp64 evaluation is itself held to the oracle's closed form on
+  the sampled matrices (rows agree to 1e-12), so a batching or indexing error
+  in any matrix of any launch shows up.
+At DiT-15B (W, M and G take 180 GB) there is no room for that second copy, and
+only the sampled matrices get a direction output (NULL entries for the others).
 """
 import os
 import sys
@@ -45,6 +53,10 @@ NO_COPY = (4,)               # too large for a second copy of W and M
 REFRESH_SAMPLE = {wi: tuple(range(5)) + tuple(range(5 * (synth.WORKLOADS[wi].blocks - 1),
                                                      5 * synth.WORKLOADS[wi].blocks)) for wi in (1, 2, 3)}
 REFRESH_SAMPLE[4] = (0, 1, 2, 4, 5 * (synth.WORKLOADS[4].blocks - 1) + 3)
+# the fp64 GPU evaluations that check every matrix, against the oracle on the
+# same exact inputs (sampled rows): both are fp64, so they agree to rounding
+PIN_NS5 = 1e-12
+PIN_ROWWISE = 1e-12
 
 
 def make_set(wi, step):
@@ -65,10 +77,13 @@ def config(WL, precise=0):
                               param_dtype=prm.BF16, grad_dtype=prm.BF16, ns_precise=precise)
 
 
-def run(wi, step, sample, precise=0):
+def run(wi, step, sample, precise=0, every=None):
     """One step at the given t over the whole set; returns host copies of the
     sampled matrices' inputs and outputs, and (up to DiT-9B) checks the debug
-    step against the timed one bitwise."""
+    step against the timed one bitwise.  ``every(i, M_i, D_i)`` (device
+    tensors after the step) is called for every matrix that has a direction
+    output (with the host inputs of the sampled ones); its results come back
+    as a dict."""
     WL = synth.WORKLOADS[wi]
     cfg = config(WL, precise)
     shapes = list(WL.shapes)
@@ -94,9 +109,15 @@ def run(wi, step, sample, precise=0):
             assert torch.equal(a, b), "timed step differs from the debug step"
         del W2, M2
     out = {i: (pc.to_host(W[i]), pc.to_host(M[i]), pc.to_host(D[i])) for i in sample}
+    checked = {}
+    if every is not None:
+        print(f"[fullsize] {WL.name} t={step}: checking every matrix", flush=True)
+        for i in range(len(shapes)):
+            if D[i] is not None:
+                checked[i] = every(i, M[i], D[i], host_in)
     del W, M, G, D
     torch.cuda.empty_cache()
-    return cfg, host_in, out
+    return cfg, host_in, out, checked
 
 
 def oriented_rows(A, m, n, rows):
@@ -121,6 +142,66 @@ def check_rows(WL, cfg, i, rows, Do_rows, host_in, out, tol):
     assert slack <= 1.0, f"matrix {i}: W outside the rounding bound ({slack:.3f})"
 
 
+def oriented64(A, m, n):
+    """Oriented fp64 copy of a device matrix (stored rows if m <= n, else columns)."""
+    return (A if m <= n else A.t()).to(torch.float64).contiguous()
+
+
+def ns5_fp64(U, m, n, oc):
+    """s(m, n) X_5 for the oriented U: the five-iteration map of eq.
+    (app-ns-recurrence) in fp64 torch matrix products on the GPU, a check of
+    every matrix of a set (the CPU oracle takes too long for all of them)."""
+    a, b, c = oc.coeffs
+    X = oriented64(U, m, n)
+    X = X / (torch.linalg.vector_norm(X) + oc.eps_ns)
+    for _ in range(po.NS_ITERS):
+        A = torch.mm(X, X.t().contiguous())
+        B = b * A + c * torch.mm(A, A)
+        X = a * X + torch.mm(B, X)
+    return po.shape_scale(m, n, oc.scale_mode) * X
+
+
+def rownorm_fp64(U, m, n, oc):
+    """gamma s(m, n) RowNorm of the oriented U (eq. rownorm), fp64 on the GPU."""
+    X = oriented64(U, m, n)
+    nu = torch.linalg.vector_norm(X, dim=1).clamp_min(oc.eps_rownorm)
+    return (po.shape_scale(m, n, oc.scale_mode) * oc.gamma) * X / nu[:, None]
+
+
+def every_matrix(WL, oc, ref, rows_of):
+    """Callback for ``run``: D of matrix i against ``ref`` evaluated from the
+    step's own new momentum (matrix and worst-row error); for a sampled matrix
+    also ``ref`` evaluated from the exact fp64 momentum of the host inputs at
+    the sampled rows, which the test holds to the oracle."""
+    def f(i, Mi, Di, host_in):
+        m, n = WL.shapes[i]
+        R = ref(Mi, m, n, oc)
+        Dg = oriented64(Di, m, n)
+        diff = torch.linalg.vector_norm(Dg - R, dim=1)
+        den = torch.linalg.vector_norm(R, dim=1)
+        err = float(torch.linalg.vector_norm(diff) / torch.linalg.vector_norm(den))
+        worst = float((diff / den.clamp_min(1e-300)).max())
+        del R, Dg, diff, den
+        exact = None
+        if i in rows_of:
+            _, M0, G = host_in[i]
+            Ue = torch.tensor(po.momentum_update(M0, G, oc.beta), dtype=torch.float64, device="cuda")
+            exact = ref(Ue, m, n, oc)[torch.as_tensor(rows_of[i], device="cuda")].cpu().numpy()
+            del Ue
+        return err, worst, exact
+    return f
+
+
+def check_every(WL, checked, tol):
+    errs = {i: e for i, (e, _, _) in checked.items()}
+    worst = {i: w for i, (_, w, _) in checked.items()}
+    ie, iw = max(errs, key=errs.get), max(worst, key=worst.get)
+    print(f"  every matrix ({len(checked)}): largest D err {errs[ie]:.3e} (matrix {ie} {WL.shapes[ie]}), "
+          f"worst row {worst[iw]:.3e} (matrix {iw})", flush=True)
+    assert errs[ie] <= tol, f"matrix {ie}: D err {errs[ie]:.3e} > {tol}"
+    assert worst[iw] <= tol, f"matrix {iw}: worst row err {worst[iw]:.3e} > {tol}"
+
+
 @pytest.mark.parametrize("wi,precise", [(wi, 0) for wi in SETS] + [(1, 1), (2, 1)],
                          ids=[synth.WORKLOADS[i].name for i in SETS] + ["dit-1.3b-precise", "dit-4b-precise"])
 def test_refresh_step_sampled_rows(wi, precise):
@@ -128,17 +209,25 @@ def test_refresh_step_sampled_rows(wi, precise):
     plain iterations for every matrix) on DiT-1.3B and DiT-4B."""
     WL = synth.WORKLOADS[wi]
     sample = list(REFRESH_SAMPLE[wi])             # matrices of the first and last block
-    cfg, host_in, out = run(wi, 0, sample, precise)
-    oc = pc.oracle_config(cfg)
     rng = np.random.default_rng(7)
+    rows_of = {i: np.sort(rng.choice(min(WL.shapes[i]), 48, replace=False)) for i in sample}
+    oc = pc.oracle_config(config(WL, precise))
+    every = None if wi in NO_COPY else every_matrix(WL, oc, ns5_fp64, rows_of)
+    cfg, host_in, out, checked = run(wi, 0, sample, precise, every)
     for i in sample:
         m, n = WL.shapes[i]
         W0, M0, G = host_in[i]
         U = po.momentum_update(M0, G, oc.beta)
         X = po.orient(U)
-        rows = np.sort(rng.choice(X.shape[0], 48, replace=False))
+        rows = rows_of[i]
         Do = po.shape_scale(m, n, oc.scale_mode) * po.ns5_rows_closed_form(X, rows, oc.eps_ns, oc.coeffs)
         check_rows(WL, cfg, i, rows, Do, host_in, out, pc.TOL_NS5)
+        if checked:
+            pin = pc.rel(checked[i][2], Do)
+            print(f"    fp64 GPU map vs oracle closed form, sampled rows: {pin:.1e}", flush=True)
+            assert pin <= PIN_NS5, f"matrix {i}: the fp64 check map disagrees with the oracle ({pin:.1e})"
+    if checked:
+        check_every(WL, checked, pc.TOL_NS5)
 
 
 @pytest.mark.parametrize("wi", SETS, ids=[synth.WORKLOADS[i].name for i in SETS])
@@ -148,15 +237,21 @@ def test_rowwise_step_sampled_rows(wi):
     sample = list(range(5)) + list(range(5 * (L - 1), 5 * L))   # first and last block
     if wi in NO_COPY:
         sample = list(range(5)) + [5 * (L - 1) + 3]               # and the last MLP down only
-    cfg, host_in, out = run(wi, 1, sample)
-    oc = pc.oracle_config(cfg)
     rng = np.random.default_rng(8)
+    rows_of = {i: np.sort(rng.choice(min(WL.shapes[i]), 64, replace=False)) for i in sample}
+    oc = pc.oracle_config(config(WL))
+    every = None if wi in NO_COPY else every_matrix(WL, oc, rownorm_fp64, rows_of)
+    cfg, host_in, out, checked = run(wi, 1, sample, 0, every)
     for i in sample:
         m, n = WL.shapes[i]
         W0, M0, G = host_in[i]
         U = po.momentum_update(M0, G, oc.beta)
-        r = min(m, n)
-        rows = np.sort(rng.choice(r, 64, replace=False))
+        rows = rows_of[i]
         Xr = oriented_rows(U, m, n, rows)
         Do = po.shape_scale(m, n, oc.scale_mode) * oc.gamma * po.rownorm(Xr, oc.eps_rownorm)
         check_rows(WL, cfg, i, rows, Do, host_in, out, pc.TOL_ROWWISE)
+        if checked:
+            pin = pc.rel(checked[i][2], Do)
+            assert pin <= PIN_ROWWISE, f"matrix {i}: the fp64 check map disagrees with the oracle ({pin:.1e})"
+    if checked:
+        check_every(WL, checked, pc.TOL_ROWWISE)
