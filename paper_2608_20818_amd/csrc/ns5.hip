@@ -183,14 +183,10 @@ __global__ __launch_bounds__(256) void ns_alpha_kernel(const MatDesc* __restrict
 // ---------------------------------------------------------------------------
 namespace gemm {
 constexpr int BM = kNsTile, BN = kNsTile, BK = 64;
-#ifndef PRM_GEMM_WAVES_N
-#define PRM_GEMM_WAVES_N 2
-#endif
-// waves: 2 along the tile rows x WAVES_N along the columns.  2 x 2 (one wave
-// per SIMD, 128 x 128 per wave) is the default; 2 x 4 (two waves per SIMD,
-// 128 x 64 each) reads 1.5x more fragment bytes from LDS per MFMA and measured
-// about 2% slower over the DiT-4B weight set.
-constexpr int WAVES_M = 2, WAVES_N = PRM_GEMM_WAVES_N, NWAVES = WAVES_M * WAVES_N;
+// waves: 2 x 2, one per SIMD, each owning 128 x 128 of the tile.  (2 x 4, two
+// waves per SIMD at 128 x 64 each, reads 1.5x more fragment bytes from LDS per
+// MFMA and measured about 2% slower over the DiT-4B weight set.)
+constexpr int WAVES_M = 2, WAVES_N = 2, NWAVES = WAVES_M * WAVES_N;
 constexpr int NTHREADS = 64 * NWAVES;
 constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
 constexpr int MI = WM / 32, NI = WN / 32;
@@ -448,12 +444,12 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   // Compute one stage from `cur` while streaming stage `knext` (if >= 0) into
   // `nxt`.  The vector-memory path accepts about one 1 KB wave load per 16
   // cycles, so the wave's loads are spread between MFMA sub-groups (a quarter
-  // at the start, the rest over the first three k-steps) instead of stalling
+  // at the start, the rest over the first two k-steps) instead of stalling
   // the in-order issue behind a burst.  Sub-group i (row block i) also reads the
   // next k-step's A fragment i and, for i < NI, its B fragment i.
-  // FOLD (apply): 0 none; f >= 1: the stage holds this wave's output block
-  // columns 2 (f - 1) and 2 (f - 1) + 1 as k
-  // (one stage per wave, WN == BK): `fold` selects it at run time instead
+  // FOLD: 0 none; f = 1 or 2: the stage holds, as k, the wave's output block
+  // columns (apply) or rows (split product) 2 (f - 1) and 2 (f - 1) + 1, whose
+  // diagonal term is folded in when `fold` is set.
   // MORE: 1 a next stage exists, 0 none (the tile's last stage), -1 decided at
   // run time from knext; static where possible, so the main loop has no branch
   auto stage_compute = [&](const char* cur, char* nxt, int knext, auto foldc, bool fold, auto morec) __attribute__((always_inline)) {
@@ -483,12 +479,11 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
     };
     // a quarter of the loads at the start, the rest spread over the sub-groups
     // of the first DMA_KSTEPS k-steps (sub-group s issues loads
-    // [DMA0 + REM s / NS, DMA0 + REM (s + 1) / NS))
-#ifndef PRM_DMA_KSTEPS
-#define PRM_DMA_KSTEPS 2
-#endif
-    constexpr int DMA0 = NDMA / 4, REM = NDMA - DMA0, NS = PRM_DMA_KSTEPS * MI;
-    static_assert(PRM_DMA_KSTEPS >= 1 && PRM_DMA_KSTEPS <= 3, "loads must be issued before the last k-step");
+    // [DMA0 + REM s / NS, DMA0 + REM (s + 1) / NS)); spreading them over one
+    // or three k-steps instead measured equal or slower
+    constexpr int DMA_KSTEPS = 2;
+    constexpr int DMA0 = NDMA / 4, REM = NDMA - DMA0, NS = DMA_KSTEPS * MI;
+    static_assert(DMA_KSTEPS >= 1 && DMA_KSTEPS <= 3, "loads must be issued before the last k-step");
     if (more) {
 #pragma unroll
       for (int q = 0; q < DMA0; ++q) dma1(nxt, sgn, kn, q);
@@ -505,7 +500,7 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
 #pragma unroll
       for (int i = 0; i < (ks == 3 ? MI - NDEF : MI); ++i) {  // sub-group: row block i, NI MFMAs
         if (ks < 3) {
-          if (ks < PRM_DMA_KSTEPS && more) {
+          if (ks < DMA_KSTEPS && more) {
             const int slot = ks * MI + i;
 #pragma unroll
             for (int q = DMA0 + REM * slot / NS; q < DMA0 + REM * (slot + 1) / NS; ++q) dma1(nxt, sgn, kn, q);
@@ -570,31 +565,24 @@ __global__ __launch_bounds__(gemm::NTHREADS, 1) void ns_gemm_kernel(const MatDes
   const int kfold = (KIND == GEMM_APPLY) ? (int)((col0 + wn * WN) / BK)
                     : (KIND == GEMM_SPROD) ? (int)((row0 + wm * WM) / BK) : nk;
   int kt = 0;
-  if constexpr (KIND == GEMM_APPLY && WN == BK) {
-    // one stage: a run-time flag in a single loop (J is static either way)
-    static_assert(NSEG == 1, "one segment with this wave layout");
-    constexpr std::integral_constant<int, -1> fold_rt{};
-    for (; kt < nk; kt += 2) stage_pair(kt, fold_rt, fold_rt, kt == kfold, kt + 1 == kfold, more_rt);
-  } else {
-    // two stages (a stage pair): it runs between two plain loops, since one
-    // loop body holding both variants spills.  The pairs before the last one
-    // always stream a next stage; the last pair (kt = NK - 2) runs on its own.
-    // With several segments the fold pair recurs in each (the diagonal term
-    // applies to every part of the iterate).
-    constexpr bool FOLDS = KIND == GEMM_APPLY || KIND == GEMM_SPROD;
-    if constexpr (FOLDS) {
-      static_assert(WN == 2 * BK && WM == 2 * BK, "a wave's output columns (rows) span two stages");
+  // The fold (apply, split product) takes two stages (a stage pair), which run
+  // between two plain loops, since one loop body holding both variants spills.
+  // The pairs before the last one always stream a next stage; the last pair
+  // (kt = NK - 2) runs on its own.  With several segments the fold pair recurs
+  // in each (the diagonal term applies to every part of the iterate).
+  constexpr bool FOLDS = KIND == GEMM_APPLY || KIND == GEMM_SPROD;
+  if constexpr (FOLDS) {
+    static_assert(WN == 2 * BK && WM == 2 * BK, "a wave's output columns (rows) span two stages");
 #pragma unroll
-      for (int sg = 0; sg < NSEG; ++sg) {
-        const int kf = sg * nk + (kfold & ~1);  // kfold < nk
-        for (; kt < kf; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
-        stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, true, true, more_rt);
-        kt += 2;
-      }
+    for (int sg = 0; sg < NSEG; ++sg) {
+      const int kf = sg * nk + (kfold & ~1);  // kfold < nk
+      for (; kt < kf; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
+      stage_pair(kt, std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, true, true, more_rt);
+      kt += 2;
     }
-    for (; kt < NK - 2; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
-    if (kt < NK) stage_pair(kt, nofold, nofold, false, false, more_no);
   }
+  for (; kt < NK - 2; kt += 2) stage_pair(kt, nofold, nofold, false, false, more_yes);
+  if (kt < NK) stage_pair(kt, nofold, nofold, false, false, more_no);
 
   deferred();
   // ---- epilogue ----
